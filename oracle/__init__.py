@@ -1,0 +1,19 @@
+"""fp64 CPU oracle for fused scaled-dot-product attention, forward and backward.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path imports, calls or links
+this package: only the test suite, the smoke check and the CPU-baseline leg of
+the benchmark may use it.  It shares no code with the HIP library.
+
+The oracle is the plain definition of attention (whole-row two-pass softmax in
+fp64), not the tiled online-softmax method the GPU runs.  Every function is
+pinned by the CPU tests in ``tests/test_oracle.py`` against closed forms,
+invariants, finite differences, a pure-Python brute force and torch's own fp64
+SDPA; no function is left "parity unpinned".
+"""
+from .attention import (
+    attention_forward,
+    attention_backward,
+    attention_probs,
+)
+
+__all__ = ["attention_forward", "attention_backward", "attention_probs"]

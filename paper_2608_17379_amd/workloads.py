@@ -1,0 +1,126 @@
+"""Seeded synthetic attention workloads.
+
+This module only draws inputs; it holds none of the attention arithmetic, so
+both the HIP library's tests and the fp64 oracle can be fed from it without
+sharing any computation.
+
+Every input is i.i.d. N(0, 1) drawn in fp32 on the CPU and rounded to bf16
+with round-to-nearest-even (torch's cast), so the GPU and the oracle see the
+same bits.  One ``torch.Generator`` seeded with ``seed`` draws, in order: the
+packed sequence lengths (variable-length workload only), then Q, K, V and dO.
+The long-sequence workload multiplies Q and K by 2 after the cast (exact in
+bf16), which makes the softmax rows peaky (logit std about 4).
+
+Shapes follow the attention workloads of PTXBench (Appendix A, "Workloads"
+and "Generalization attention workloads"): bf16 Q, K, V of shape
+[B, H, S, D], an fp32 log-sum-exp of shape [B, H, S], causal variants with a
+lower-triangular mask, grouped-query variants with fewer key/value heads, and
+ragged causal prefill over packed sequences.  The five sizes below are the
+ones this library is measured on; the paper's own trace files are not
+available, so these synthetic tensors stand in for them.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import torch
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int            # batch (fixed-length) or number of sequences (packed)
+    Hq: int
+    Hkv: int
+    S: int            # sequence length (fixed-length) or max length (packed)
+    D: int
+    causal: bool
+    qk_mult: float = 1.0
+    varlen: bool = False
+    len_lo: int = 0   # packed: lengths drawn uniformly in [len_lo, len_hi]
+    len_hi: int = 0
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / math.sqrt(self.D)
+
+
+WORKLOADS = {
+    "mha_b1_h1_s128_d64": Workload("mha_b1_h1_s128_d64", 1, 1, 1, 128, 64, False),
+    "mha_causal_b4_h16_s2048_d128": Workload(
+        "mha_causal_b4_h16_s2048_d128", 4, 16, 16, 2048, 128, True),
+    "gqa_causal_b2_hq32_hkv8_s4096_d128": Workload(
+        "gqa_causal_b2_hq32_hkv8_s4096_d128", 2, 32, 8, 4096, 128, True),
+    "long_causal_b1_h16_s16384_d128_qk2": Workload(
+        "long_causal_b1_h16_s16384_d128_qk2", 1, 16, 16, 16384, 128, True, qk_mult=2.0),
+    "varlen_causal_n8_l512_8192_h32_d64": Workload(
+        "varlen_causal_n8_l512_8192_h32_d64", 8, 32, 32, 8192, 64, True,
+        varlen=True, len_lo=512, len_hi=8192),
+}
+
+# The configuration the headline throughput is quoted on.
+HEADLINE = "mha_causal_b4_h16_s2048_d128"
+
+
+@dataclass
+class Inputs:
+    workload: Workload
+    q: torch.Tensor
+    k: torch.Tensor
+    v: torch.Tensor
+    do: torch.Tensor
+    cu_seqlens: Optional[List[int]] = None
+
+    @property
+    def total(self) -> int:
+        return self.q.shape[0] if self.cu_seqlens is not None else 0
+
+    @property
+    def max_seqlen(self) -> int:
+        if self.cu_seqlens is None:
+            return self.q.shape[2]
+        cu = self.cu_seqlens
+        return max(b - a for a, b in zip(cu, cu[1:]))
+
+
+def _randn_bf16(gen: torch.Generator, shape) -> torch.Tensor:
+    return torch.randn(*shape, generator=gen, dtype=torch.float32).to(torch.bfloat16)
+
+
+def make_inputs(w: Workload, seed: int = 0, lengths: Optional[List[int]] = None) -> Inputs:
+    """Draw the bf16 inputs of workload ``w`` on the CPU.
+
+    ``lengths`` overrides the drawn packed sequence lengths (tests use it for
+    ragged and empty sequences); it is ignored for fixed-length workloads.
+    """
+    gen = torch.Generator().manual_seed(seed)
+    if w.varlen:
+        if lengths is None:
+            lengths = torch.randint(w.len_lo, w.len_hi + 1, (w.B,), generator=gen).tolist()
+        cu = [0]
+        for n in lengths:
+            cu.append(cu[-1] + int(n))
+        t = cu[-1]
+        q = _randn_bf16(gen, (t, w.Hq, w.D))
+        k = _randn_bf16(gen, (t, w.Hkv, w.D))
+        v = _randn_bf16(gen, (t, w.Hkv, w.D))
+        do = _randn_bf16(gen, (t, w.Hq, w.D))
+    else:
+        cu = None
+        q = _randn_bf16(gen, (w.B, w.Hq, w.S, w.D))
+        k = _randn_bf16(gen, (w.B, w.Hkv, w.S, w.D))
+        v = _randn_bf16(gen, (w.B, w.Hkv, w.S, w.D))
+        do = _randn_bf16(gen, (w.B, w.Hq, w.S, w.D))
+    if w.qk_mult != 1.0:
+        q = q * w.qk_mult
+        k = k * w.qk_mult
+    return Inputs(w, q, k, v, do, cu)
+
+
+def small(name: str, B: int, Hq: int, Hkv: int, S: int, D: int, causal: bool,
+          varlen: bool = False, qk_mult: float = 1.0) -> Workload:
+    """An ad-hoc workload for shape sweeps (same drawing recipe)."""
+    return Workload(name, B, Hq, Hkv, S, D, causal, qk_mult=qk_mult, varlen=varlen,
+                    len_lo=1, len_hi=max(1, S))

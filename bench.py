@@ -1,0 +1,259 @@
+#!/usr/bin/env python3
+"""Throughput of fused attention forward + backward on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME]
+
+A step is one forward (attn_fwd) and one backward (attn_bwd_phases with the
+Delta/dQ phase, then the dK/dV phase: together exactly attn_bwd) over one
+batch of seeded synthetic bf16 inputs already resident in HBM.  W untimed
+steps, then K timed steps between two synchronisations; one JSON line is
+printed.
+
+FLOP convention: forward 4*B*Hq*S^2*D (halved when causal; packed input sums
+L^2 over sequences), backward 2.5x forward.  TFLOP/s = (forward + backward
+FLOP) / step time.  Peak: 2516.6 TFLOP/s dense bf16 MFMA (256 CUs x 2.4 GHz
+x 4096 FLOP/clock/CU).
+
+The roofline object is for the kernel with the largest average duration.
+Each kernel's average duration comes from HIP events recorded between the
+launches inside the timed steps (all on the stream the library launches on).
+Per-launch algorithmic FLOP of each kernel:
+  fwd_kernel       2 GEMMs  (S = QK^T, O = PV)            = F
+  bwd_dq_kernel    3 GEMMs  (S, dP = dO V^T, dQ = dS K)   = 1.5 F
+  bwd_dkdv_kernel  4 GEMMs  (S, dP, dV = P^T dO, dK)      = 2 F
+with F the forward FLOP above.  `traffic` (HBM bytes per launch from
+rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a copy-kernel calibration) is
+read from profiles/traffic.json when that file was taken on the current
+kernel source, else null.
+
+The CPU baseline times the fp64 oracle (test infrastructure, used here only
+for this leg) on a bounded sample of the same workload: whole (batch, head)
+slices, forward + backward, until about --cpu-seconds have elapsed.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6
+METRIC = "attention fwd/bwd TFLOP/s + % bf16 MFMA peak, B4 H16 S2048 D128 causal"
+KERNELS = ("fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel")
+GEMMS = {"fwd_kernel": 2, "bwd_dq_kernel": 3, "bwd_dkdv_kernel": 4}
+KERNEL_SOURCES = {"fwd_kernel": "attn_fwd.hip", "bwd_dq_kernel": "attn_bwd.hip",
+                  "bwd_dkdv_kernel": "attn_bwd.hip"}
+
+
+def fwd_flops(w, cu_seqlens=None) -> float:
+    """4 * Hq * D * sum(L^2) (x1/2 causal), as in the module docstring."""
+    if cu_seqlens is not None:
+        sq = sum((b - a) ** 2 for a, b in zip(cu_seqlens, cu_seqlens[1:]))
+        f = 4.0 * w.Hq * w.D * sq
+    else:
+        f = 4.0 * w.B * w.Hq * w.S * w.S * w.D
+    return f * (0.5 if w.causal else 1.0)
+
+
+def source_sha(kernel: str) -> str:
+    path = os.path.join(ROOT, "paper_2608_17379_amd", "csrc", KERNEL_SOURCES[kernel])
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def load_traffic(kernel: str, workload: str):
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        rec = json.load(open(path))[f"{kernel}:{workload}"]
+    except (OSError, KeyError, ValueError):
+        return None
+    if rec.get("source_sha") != source_sha(kernel):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(w, x, seconds: float):
+    """Oracle (fp64, CPU) forward + backward on whole head slices."""
+    import torch
+    import oracle
+    n_done, flop, t0 = 0, 0.0, time.perf_counter()
+    G = w.Hq // w.Hkv
+    slices = [(b, g) for b in range(w.B) for g in range(w.Hkv)] if not w.varlen else \
+        [(s, g) for s in range(w.B) for g in range(w.Hkv)]
+    for seg, g in slices:
+        hs = list(range(g * G, (g + 1) * G))
+        if w.varlen:
+            a, b = x.cu_seqlens[seg], x.cu_seqlens[seg + 1]
+            q, k, v, do = x.q[a:b, hs], x.k[a:b, [g]], x.v[a:b, [g]], x.do[a:b, hs]
+            cu = [0, b - a]
+            f = 4.0 * G * w.D * (b - a) ** 2 * (0.5 if w.causal else 1.0)
+        else:
+            q, k, v, do = (x.q[seg:seg + 1, hs], x.k[seg:seg + 1, [g]], x.v[seg:seg + 1, [g]],
+                           x.do[seg:seg + 1, hs])
+            cu = None
+            f = 4.0 * G * w.S * w.S * w.D * (0.5 if w.causal else 1.0)
+        oracle.attention_forward(q, k, v, w.causal, w.scale, cu_seqlens=cu)
+        oracle.attention_backward(q, k, v, do, w.causal, w.scale, cu_seqlens=cu)
+        n_done += 1
+        flop += 3.5 * f
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    return {
+        "value": round(flop / dt / 1e12, 6),
+        "unit": "TFLOP/s",
+        "cores": torch.get_num_threads(),
+        "kind": "oracle",
+        "sample": f"{n_done} of {len(slices)} key/value-head slices ({G} query heads each) of "
+                  f"{w.name}, fp64 forward + backward, {dt:.1f} s",
+    }
+
+
+def copy_calibration(nbytes: int, reps: int) -> None:
+    """A plain device copy of known size, for scaling HBM byte counters."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes, "reps": reps}), flush=True)
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the attention path is not sharded across GPUs).", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2608_17379_amd import attn
+    from paper_2608_17379_amd import workloads as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration, max(1, args.steps))
+        return 0
+
+    w = wl.WORKLOADS[args.workload or wl.HEADLINE]
+    x = wl.make_inputs(w, 0)
+    dev = torch.device("cuda", 0)
+    q, k, v, do = (t.to(dev) for t in (x.q, x.k, x.v, x.do))
+    o, dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    cu = None
+    if w.varlen:
+        cu = torch.tensor(x.cu_seqlens, dtype=torch.int32, device=dev)
+        lse = torch.empty(w.Hq, q.shape[0], dtype=torch.float32, device=dev)
+    else:
+        lse = torch.empty(w.B, w.Hq, w.S, dtype=torch.float32, device=dev)
+    ws = attn.workspace_for(q, k, cu)
+    ms_len = x.max_seqlen
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        if cu is None:
+            attn.attn_fwd(q, k, v, o, lse, w.causal, w.scale)
+        else:
+            attn.attn_fwd_varlen(q, k, v, o, lse, cu, ms_len, w.causal, w.scale,
+                                 cu_seqlens_host=x.cu_seqlens)
+        if ev is not None:
+            ev[1].record()
+        for i, ph in enumerate((attn.ATTN_BWD_DQ, attn.ATTN_BWD_DKDV)):
+            if cu is None:
+                attn.attn_bwd_phases(q, k, v, o, lse, do, dq, dk, dv, w.causal, w.scale, ws, ph)
+            else:
+                attn.attn_bwd_varlen_phases(q, k, v, o, lse, do, dq, dk, dv, cu, ms_len, w.causal,
+                                            w.scale, ws, ph, cu_seqlens_host=x.cu_seqlens)
+            if ev is not None:
+                ev[2 + i].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        step(evs[i])
+    end.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(end) / args.steps
+    kern_ms = {
+        name: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps
+        for j, name in enumerate(KERNELS)
+    }
+    for t in (o, lse, dq, dk, dv):
+        if not torch.isfinite(t.float()).all():
+            print("non-finite output", file=sys.stderr)
+            return 1
+
+    F = fwd_flops(w, x.cu_seqlens)
+    total = 3.5 * F
+    value = total / (ms_step * 1e-3) / 1e12
+    dom = max(KERNELS, key=lambda n: kern_ms[n])
+    achieved = GEMMS[dom] / 2 * F / (kern_ms[dom] * 1e-3) / 1e12
+    fwd_ms = kern_ms["fwd_kernel"]
+    bwd_ms = kern_ms["bwd_dq_kernel"] + kern_ms["bwd_dkdv_kernel"]
+    cfg = {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "S": w.S, "D": w.D,
+           "causal": w.causal, "seed": 0}
+    if w.varlen:
+        cfg["seq_lens"] = [b - a for a, b in zip(x.cu_seqlens, x.cu_seqlens[1:])]
+    rec = {
+        "metric": METRIC if w.name == wl.HEADLINE else f"attention fwd/bwd TFLOP/s, {w.name}",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded i.i.d. N(0,1) bf16)",
+        "config": cfg,
+        "pct_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
+        "fwd_tflops": round(F / (fwd_ms * 1e-3) / 1e12, 2),
+        "bwd_tflops": round(2.5 * F / (bwd_ms * 1e-3) / 1e12, 2),
+        "fwd_pct_peak": round(100 * F / (fwd_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+        "bwd_pct_peak": round(100 * 2.5 * F / (bwd_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+        "kernel_ms": {n: round(t, 4) for n, t in kern_ms.items()},
+        "roofline": {
+            "kernel": dom,
+            "bound": "mfma",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": load_traffic(dom, w.name),
+        },
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(w, x, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

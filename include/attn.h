@@ -1,0 +1,151 @@
+/*
+ * attn.h - fused scaled-dot-product attention, forward and backward, for AMD
+ * Instinct MI355X (gfx950).  C ABI of libattn.so.
+ *
+ * What is computed (PTXBench, Appendix A, paragraph "Workloads"): the forward
+ * takes bf16 Q, K, V and returns the bf16 attention output O (same shape as Q)
+ * and the fp32 log-sum-exp of every query row; the backward additionally takes
+ * O, its upstream gradient dO and the log-sum-exp, and returns bf16 dQ, dK,
+ * dV.  Causal variants apply a lower-triangular mask: key j is visible to
+ * query i iff j <= i.  Grouped-query variants ("Generalization attention
+ * workloads") let Hq query heads share Hkv key/value heads: query head h reads
+ * key/value head h / (Hq/Hkv), and dK, dV are summed over each group.  The
+ * ragged-prefill variant packs several sequences of different lengths; no
+ * attention crosses a sequence boundary and positions are local to each
+ * sequence.
+ *
+ *   O   = softmax(scale * Q K^T + mask) V
+ *   LSE = log(sum_j exp(scale * q_i . k_j))  over the visible keys j, natural
+ *         log, scale included (the L_i = m_i + log l_i of the epilogue of the
+ *         corrected FlashAttention-3 Algorithm 2, Appendix A)
+ *
+ * Layouts (all tensors contiguous, bf16 = raw IEEE bfloat16 bits):
+ *   fixed length : q, o, dO, dq   [B, Hq,  S, D]     lse [B, Hq, S] fp32
+ *                  k, v, dk, dv   [B, Hkv, S, D]
+ *   packed       : q, o, dO, dq   [T, Hq,  D]        lse [Hq, T] fp32
+ *                  k, v, dk, dv   [T, Hkv, D]
+ *                  sequence s owns rows cu_seqlens[s] .. cu_seqlens[s+1]-1;
+ *                  cu_seqlens is an int32 device array of nseq+1 entries,
+ *                  non-decreasing, starting at 0 and ending at T.
+ *
+ * Ownership: every pointer is device memory owned by the caller.  Inputs are
+ * read only; outputs are fully overwritten (never accumulated into).  The
+ * library allocates and frees nothing; the backward's scratch space is a
+ * caller-provided workspace of attn_bwd_workspace_size() bytes.
+ *
+ * Asynchrony: all work is enqueued on `stream` (0 = the null stream).  No
+ * call synchronises or copies between host and device; the caller
+ * synchronises before reading results or reusing buffers.
+ *
+ * Errors: every call validates its arguments on the host before touching the
+ * GPU and returns ATTN_OK or a negative attn_status_t; nothing aborts.  The
+ * library never reads device memory on the host, so it cannot check the
+ * contents of cu_seqlens: the kernels clamp out-of-range offsets so that a
+ * bad array cannot make them access memory outside the tensors, but the
+ * results are then meaningless (the Python binding checks the array on the
+ * host).  A problem with no rows (B == 0, S == 0, nseq == 0 or T == 0) is a
+ * no-op that returns ATTN_OK; its pointers may then be null.
+ */
+#ifndef ATTN_H
+#define ATTN_H
+
+#include <stddef.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ATTN_OK = 0,
+  ATTN_ERR_NULL = -1,       /* a required pointer is null */
+  ATTN_ERR_SHAPE = -2,      /* a size is negative, Hq/Hkv < 1, or too large */
+  ATTN_ERR_GQA = -3,        /* Hq is not a multiple of Hkv */
+  ATTN_ERR_HEAD_DIM = -4,   /* D is not 64 or 128 */
+  ATTN_ERR_ALIGN = -5,      /* a pointer is not 16-byte aligned */
+  ATTN_ERR_WORKSPACE = -6,  /* workspace null or smaller than required */
+  ATTN_ERR_HIP = -7,        /* a kernel launch failed (hipGetLastError) */
+  ATTN_ERR_VALUE = -8       /* scale not finite, causal not 0/1, max_seqlen < 1,
+                               or a bad backward phase mask */
+} attn_status_t;
+
+/*
+ * Forward, fixed length.  q [B,Hq,S,D], k/v [B,Hkv,S,D] in; o [B,Hq,S,D] and
+ * lse [B,Hq,S] out.  causal is 0 or 1; scale is the softmax scale (1/sqrt(D)
+ * in every measured workload).
+ */
+int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
+             int B, int Hq, int Hkv, int S, int D, int causal, float scale,
+             hipStream_t stream);
+
+/* Bytes of backward workspace for the fixed-length layout (fp32 Delta). */
+size_t attn_bwd_workspace_size(int B, int Hq, int Hkv, int S, int D);
+
+/*
+ * Backward, fixed length.  Consumes q, k, v, the forward's o and lse, and
+ * dO; writes dq [B,Hq,S,D] and dk, dv [B,Hkv,S,D] (dk, dv summed over each
+ * query-head group).  Delta_i = sum_d dO_id * O_id is precomputed into the
+ * workspace; P is recomputed from lse.  The gradients are of the loss
+ * sum(dO * O) with O = attention(q, k, v).  The result is deterministic
+ * (no atomics).
+ */
+int attn_bwd(const void* q, const void* k, const void* v, const void* o,
+             const float* lse, const void* dO, void* dq, void* dk, void* dv,
+             int B, int Hq, int Hkv, int S, int D, int causal, float scale,
+             void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Forward, packed variable length (ragged prefill).  total = T rows;
+ * max_seqlen >= the longest sequence (it sizes the launch; a longer sequence
+ * is processed only up to max_seqlen rows).
+ */
+int attn_fwd_varlen(const void* q, const void* k, const void* v, void* o,
+                    float* lse, const int* cu_seqlens, int nseq,
+                    int max_seqlen, int total, int Hq, int Hkv, int D,
+                    int causal, float scale, hipStream_t stream);
+
+/* Bytes of backward workspace for the packed layout (fp32 Delta). */
+size_t attn_bwd_varlen_workspace_size(int total, int Hq, int Hkv, int D);
+
+/* Backward, packed variable length.  Same contract as attn_bwd. */
+int attn_bwd_varlen(const void* q, const void* k, const void* v,
+                    const void* o, const float* lse, const void* dO, void* dq,
+                    void* dk, void* dv, const int* cu_seqlens, int nseq,
+                    int max_seqlen, int total, int Hq, int Hkv, int D,
+                    int causal, float scale, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * The backward in separately enqueued phases, for callers that time or
+ * schedule its two kernels on their own.  `phases` is a bit mask:
+ *   ATTN_BWD_DQ   computes Delta into the workspace, then dq;
+ *   ATTN_BWD_DKDV computes dk and dv from the Delta of an ATTN_BWD_DQ phase
+ *                 enqueued earlier on the same stream with the same
+ *                 workspace and inputs.
+ * phases = ATTN_BWD_DQ | ATTN_BWD_DKDV is exactly attn_bwd / attn_bwd_varlen;
+ * any other value returns ATTN_ERR_VALUE.  Arguments are as for those calls.
+ */
+#define ATTN_BWD_DQ 1
+#define ATTN_BWD_DKDV 2
+int attn_bwd_phases(const void* q, const void* k, const void* v, const void* o,
+                    const float* lse, const void* dO, void* dq, void* dk,
+                    void* dv, int B, int Hq, int Hkv, int S, int D, int causal,
+                    float scale, void* workspace, size_t workspace_bytes,
+                    int phases, hipStream_t stream);
+int attn_bwd_varlen_phases(const void* q, const void* k, const void* v,
+                           const void* o, const float* lse, const void* dO,
+                           void* dq, void* dk, void* dv,
+                           const int* cu_seqlens, int nseq, int max_seqlen,
+                           int total, int Hq, int Hkv, int D, int causal,
+                           float scale, void* workspace,
+                           size_t workspace_bytes, int phases,
+                           hipStream_t stream);
+
+/* Static, human-readable text for a status code (never null). */
+const char* attn_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ATTN_H */

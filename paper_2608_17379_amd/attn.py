@@ -1,0 +1,275 @@
+"""ctypes binding of libattn.so (the C ABI declared in include/attn.h).
+
+Argument marshalling only: every function checks the tensors it is given
+(device, dtype, contiguity, shapes), passes raw device pointers, the sizes and
+the current HIP stream to the C entry point of the same name, and turns a
+non-zero status into ``AttnError``.  All arithmetic runs in the library's HIP
+kernels; there is no fallback of any kind, and loading fails loudly when the
+library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libattn.so")
+
+ATTN_OK = 0
+STATUS_NAMES = {
+    0: "ATTN_OK", -1: "ATTN_ERR_NULL", -2: "ATTN_ERR_SHAPE", -3: "ATTN_ERR_GQA",
+    -4: "ATTN_ERR_HEAD_DIM", -5: "ATTN_ERR_ALIGN", -6: "ATTN_ERR_WORKSPACE",
+    -7: "ATTN_ERR_HIP", -8: "ATTN_ERR_VALUE",
+}
+EXPORTS = ("attn_fwd", "attn_bwd", "attn_bwd_workspace_size", "attn_fwd_varlen",
+           "attn_bwd_varlen", "attn_bwd_varlen_workspace_size", "attn_bwd_phases",
+           "attn_bwd_varlen_phases", "attn_status_string")
+ATTN_BWD_DQ = 1
+ATTN_BWD_DKDV = 2
+
+
+class AttnError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)} ({attn_status_string(status)})")
+
+
+_lib = None
+_P, _I, _F, _Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+
+
+def lib() -> ctypes.CDLL:
+    """Load libattn.so once; raise if it is missing (no fallback exists)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2608_17379_amd.build`")
+        l = ctypes.CDLL(LIB_PATH)
+        l.attn_fwd.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _P]
+        l.attn_fwd.restype = _I
+        l.attn_bwd_workspace_size.argtypes = [_I, _I, _I, _I, _I]
+        l.attn_bwd_workspace_size.restype = _Z
+        l.attn_bwd.argtypes = [_P] * 9 + [_I] * 6 + [_F, _P, _Z, _P]
+        l.attn_bwd.restype = _I
+        l.attn_fwd_varlen.argtypes = [_P] * 6 + [_I] * 7 + [_F, _P]
+        l.attn_fwd_varlen.restype = _I
+        l.attn_bwd_varlen_workspace_size.argtypes = [_I, _I, _I, _I]
+        l.attn_bwd_varlen_workspace_size.restype = _Z
+        l.attn_bwd_varlen.argtypes = [_P] * 10 + [_I] * 7 + [_F, _P, _Z, _P]
+        l.attn_bwd_varlen.restype = _I
+        l.attn_bwd_phases.argtypes = [_P] * 9 + [_I] * 6 + [_F, _P, _Z, _I, _P]
+        l.attn_bwd_phases.restype = _I
+        l.attn_bwd_varlen_phases.argtypes = [_P] * 10 + [_I] * 7 + [_F, _P, _Z, _I, _P]
+        l.attn_bwd_varlen_phases.restype = _I
+        l.attn_status_string.argtypes = [_I]
+        l.attn_status_string.restype = ctypes.c_char_p
+        _lib = l
+    return _lib
+
+
+def attn_status_string(status: int) -> str:
+    return lib().attn_status_string(int(status)).decode()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _ptr(t: Optional[torch.Tensor], name: str, dtype=torch.bfloat16) -> int:
+    if t is None:
+        return 0
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _shape(t: torch.Tensor, want, name: str):
+    if tuple(t.shape) != tuple(want):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(want)}")
+
+
+def _check(status: int, where: str):
+    if status != ATTN_OK:
+        raise AttnError(status, where)
+
+
+# --------------------------------------------------------------------------
+# Fixed length [B, H, S, D]
+# --------------------------------------------------------------------------
+
+def attn_bwd_workspace_size(B: int, Hq: int, Hkv: int, S: int, D: int) -> int:
+    return int(lib().attn_bwd_workspace_size(B, Hq, Hkv, S, D))
+
+
+def attn_fwd(q, k, v, o, lse, causal: bool, scale: float, stream=None) -> None:
+    B, Hq, S, D = q.shape
+    Hkv = k.shape[1]
+    _shape(k, (B, Hkv, S, D), "k")
+    _shape(v, (B, Hkv, S, D), "v")
+    _shape(o, (B, Hq, S, D), "o")
+    _shape(lse, (B, Hq, S), "lse")
+    st = lib().attn_fwd(_ptr(q, "q"), _ptr(k, "k"), _ptr(v, "v"), _ptr(o, "o"),
+                        _ptr(lse, "lse", torch.float32), B, Hq, Hkv, S, D, int(bool(causal)),
+                        float(scale), _stream(stream))
+    _check(st, "attn_fwd")
+
+
+def attn_bwd_phases(q, k, v, o, lse, dO, dq, dk, dv, causal: bool, scale: float,
+                    workspace: torch.Tensor, phases: int, stream=None) -> None:
+    B, Hq, S, D = q.shape
+    Hkv = k.shape[1]
+    for t, n, hh in ((k, "k", Hkv), (v, "v", Hkv), (o, "o", Hq), (dO, "dO", Hq),
+                     (dq, "dq", Hq), (dk, "dk", Hkv), (dv, "dv", Hkv)):
+        _shape(t, (B, hh, S, D), n)
+    _shape(lse, (B, Hq, S), "lse")
+    st = lib().attn_bwd_phases(_ptr(q, "q"), _ptr(k, "k"), _ptr(v, "v"), _ptr(o, "o"),
+                               _ptr(lse, "lse", torch.float32), _ptr(dO, "dO"), _ptr(dq, "dq"),
+                               _ptr(dk, "dk"), _ptr(dv, "dv"), B, Hq, Hkv, S, D,
+                               int(bool(causal)), float(scale),
+                               _ptr(workspace, "workspace", torch.uint8), workspace.numel(),
+                               int(phases), _stream(stream))
+    _check(st, "attn_bwd_phases")
+
+
+def attn_bwd(q, k, v, o, lse, dO, dq, dk, dv, causal: bool, scale: float,
+             workspace: torch.Tensor, stream=None) -> None:
+    B, Hq, S, D = q.shape
+    Hkv = k.shape[1]
+    for t, n, hh in ((k, "k", Hkv), (v, "v", Hkv), (o, "o", Hq), (dO, "dO", Hq),
+                     (dq, "dq", Hq), (dk, "dk", Hkv), (dv, "dv", Hkv)):
+        _shape(t, (B, hh, S, D), n)
+    _shape(lse, (B, Hq, S), "lse")
+    st = lib().attn_bwd(_ptr(q, "q"), _ptr(k, "k"), _ptr(v, "v"), _ptr(o, "o"),
+                        _ptr(lse, "lse", torch.float32), _ptr(dO, "dO"), _ptr(dq, "dq"),
+                        _ptr(dk, "dk"), _ptr(dv, "dv"), B, Hq, Hkv, S, D, int(bool(causal)),
+                        float(scale), _ptr(workspace, "workspace", torch.uint8),
+                        workspace.numel(), _stream(stream))
+    _check(st, "attn_bwd")
+
+
+# --------------------------------------------------------------------------
+# Packed variable length [T, H, D]
+# --------------------------------------------------------------------------
+
+def attn_bwd_varlen_workspace_size(total: int, Hq: int, Hkv: int, D: int) -> int:
+    return int(lib().attn_bwd_varlen_workspace_size(total, Hq, Hkv, D))
+
+
+def check_cu_seqlens(cu_host: Sequence[int], total: int, max_seqlen: int) -> None:
+    """Host-side check of the offsets the library cannot read itself."""
+    cu = [int(c) for c in cu_host]
+    if not cu or cu[0] != 0 or cu[-1] != total:
+        raise ValueError("cu_seqlens must start at 0 and end at total")
+    if any(b < a for a, b in zip(cu, cu[1:])):
+        raise ValueError("cu_seqlens must be non-decreasing")
+    if any(b - a > max_seqlen for a, b in zip(cu, cu[1:])):
+        raise ValueError("a sequence is longer than max_seqlen")
+
+
+def _varlen_common(q, k, cu_seqlens, max_seqlen, cu_seqlens_host):
+    T, Hq, D = q.shape
+    Hkv = k.shape[1]
+    nseq = cu_seqlens.numel() - 1
+    host = cu_seqlens_host if cu_seqlens_host is not None else cu_seqlens.cpu().tolist()
+    check_cu_seqlens(host, T, max_seqlen)
+    return T, Hq, Hkv, D, nseq
+
+
+def attn_fwd_varlen(q, k, v, o, lse, cu_seqlens, max_seqlen: int, causal: bool, scale: float,
+                    stream=None, cu_seqlens_host: Optional[Sequence[int]] = None) -> None:
+    T, Hq, Hkv, D, nseq = _varlen_common(q, k, cu_seqlens, max_seqlen, cu_seqlens_host)
+    _shape(k, (T, Hkv, D), "k")
+    _shape(v, (T, Hkv, D), "v")
+    _shape(o, (T, Hq, D), "o")
+    _shape(lse, (Hq, T), "lse")
+    st = lib().attn_fwd_varlen(_ptr(q, "q"), _ptr(k, "k"), _ptr(v, "v"), _ptr(o, "o"),
+                               _ptr(lse, "lse", torch.float32),
+                               _ptr(cu_seqlens, "cu_seqlens", torch.int32), nseq, int(max_seqlen),
+                               T, Hq, Hkv, D, int(bool(causal)), float(scale), _stream(stream))
+    _check(st, "attn_fwd_varlen")
+
+
+def attn_bwd_varlen_phases(q, k, v, o, lse, dO, dq, dk, dv, cu_seqlens, max_seqlen: int,
+                           causal: bool, scale: float, workspace: torch.Tensor, phases: int,
+                           stream=None, cu_seqlens_host: Optional[Sequence[int]] = None) -> None:
+    T, Hq, Hkv, D, nseq = _varlen_common(q, k, cu_seqlens, max_seqlen, cu_seqlens_host)
+    for t, n, hh in ((k, "k", Hkv), (v, "v", Hkv), (o, "o", Hq), (dO, "dO", Hq),
+                     (dq, "dq", Hq), (dk, "dk", Hkv), (dv, "dv", Hkv)):
+        _shape(t, (T, hh, D), n)
+    _shape(lse, (Hq, T), "lse")
+    st = lib().attn_bwd_varlen_phases(
+        _ptr(q, "q"), _ptr(k, "k"), _ptr(v, "v"), _ptr(o, "o"), _ptr(lse, "lse", torch.float32),
+        _ptr(dO, "dO"), _ptr(dq, "dq"), _ptr(dk, "dk"), _ptr(dv, "dv"),
+        _ptr(cu_seqlens, "cu_seqlens", torch.int32), nseq, int(max_seqlen), T, Hq, Hkv, D,
+        int(bool(causal)), float(scale), _ptr(workspace, "workspace", torch.uint8),
+        workspace.numel(), int(phases), _stream(stream))
+    _check(st, "attn_bwd_varlen_phases")
+
+
+def attn_bwd_varlen(q, k, v, o, lse, dO, dq, dk, dv, cu_seqlens, max_seqlen: int, causal: bool,
+                    scale: float, workspace: torch.Tensor, stream=None,
+                    cu_seqlens_host: Optional[Sequence[int]] = None) -> None:
+    T, Hq, Hkv, D, nseq = _varlen_common(q, k, cu_seqlens, max_seqlen, cu_seqlens_host)
+    for t, n, hh in ((k, "k", Hkv), (v, "v", Hkv), (o, "o", Hq), (dO, "dO", Hq),
+                     (dq, "dq", Hq), (dk, "dk", Hkv), (dv, "dv", Hkv)):
+        _shape(t, (T, hh, D), n)
+    _shape(lse, (Hq, T), "lse")
+    st = lib().attn_bwd_varlen(_ptr(q, "q"), _ptr(k, "k"), _ptr(v, "v"), _ptr(o, "o"),
+                               _ptr(lse, "lse", torch.float32), _ptr(dO, "dO"), _ptr(dq, "dq"),
+                               _ptr(dk, "dk"), _ptr(dv, "dv"),
+                               _ptr(cu_seqlens, "cu_seqlens", torch.int32), nseq, int(max_seqlen),
+                               T, Hq, Hkv, D, int(bool(causal)), float(scale),
+                               _ptr(workspace, "workspace", torch.uint8), workspace.numel(),
+                               _stream(stream))
+    _check(st, "attn_bwd_varlen")
+
+
+# --------------------------------------------------------------------------
+# Allocating conveniences (torch allocates the outputs; the library fills them)
+# --------------------------------------------------------------------------
+
+def forward(q, k, v, causal: bool, scale: float, cu_seqlens=None, max_seqlen: int = 0,
+            cu_seqlens_host=None):
+    """Return (o, lse) for fixed-length or packed inputs."""
+    o = torch.empty_like(q)
+    if cu_seqlens is None:
+        lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
+        attn_fwd(q, k, v, o, lse, causal, scale)
+    else:
+        lse = torch.empty((q.shape[1], q.shape[0]), dtype=torch.float32, device=q.device)
+        attn_fwd_varlen(q, k, v, o, lse, cu_seqlens, max_seqlen, causal, scale,
+                        cu_seqlens_host=cu_seqlens_host)
+    return o, lse
+
+
+def workspace_for(q, k, cu_seqlens=None) -> torch.Tensor:
+    if cu_seqlens is None:
+        B, Hq, S, D = q.shape
+        n = attn_bwd_workspace_size(B, Hq, k.shape[1], S, D)
+    else:
+        T, Hq, D = q.shape
+        n = attn_bwd_varlen_workspace_size(T, Hq, k.shape[1], D)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=q.device)
+
+
+def backward(q, k, v, o, lse, dO, causal: bool, scale: float, cu_seqlens=None,
+             max_seqlen: int = 0, workspace=None, cu_seqlens_host=None):
+    """Return (dq, dk, dv) for fixed-length or packed inputs."""
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = workspace if workspace is not None else workspace_for(q, k, cu_seqlens)
+    if cu_seqlens is None:
+        attn_bwd(q, k, v, o, lse, dO, dq, dk, dv, causal, scale, ws)
+    else:
+        attn_bwd_varlen(q, k, v, o, lse, dO, dq, dk, dv, cu_seqlens, max_seqlen, causal, scale,
+                        ws, cu_seqlens_host=cu_seqlens_host)
+    return dq, dk, dv

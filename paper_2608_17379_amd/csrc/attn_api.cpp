@@ -1,0 +1,246 @@
+// C ABI of libattn.so: host-side validation, layout description and launch.
+// No call here reads device memory, allocates, copies or synchronises.
+#include <math.h>
+#include <stdint.h>
+
+#include <initializer_list>
+
+#include "../../include/attn.h"
+#include "attn_kernels.hpp"
+
+namespace {
+
+using attn::Layout;
+
+constexpr int64_t kMaxGridY = 65535;              // launch rows of tiles (128 rows each)
+
+bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
+
+// Shared checks of the scalar arguments.  Returns ATTN_OK or an error.
+int check_common(int Hq, int Hkv, int D, int causal, float scale) {
+  if (Hq < 1 || Hkv < 1) return ATTN_ERR_SHAPE;
+  if (Hq % Hkv != 0) return ATTN_ERR_GQA;
+  if (D != 64 && D != 128) return ATTN_ERR_HEAD_DIM;
+  if (causal != 0 && causal != 1) return ATTN_ERR_VALUE;
+  if (!isfinite(scale)) return ATTN_ERR_VALUE;
+  return ATTN_OK;
+}
+
+int check_rows(int64_t rows) {
+  if (rows < 0) return ATTN_ERR_SHAPE;
+  if (rows > kMaxGridY * 128) return ATTN_ERR_SHAPE;
+  return ATTN_OK;
+}
+
+Layout fixed_layout(int B, int Hq, int Hkv, int S, int D) {
+  Layout L{};
+  L.cu = nullptr;
+  L.S = S;
+  L.total = 0;
+  L.nseg = B;
+  L.Hq = Hq;
+  L.Hkv = Hkv;
+  L.group = Hq / Hkv;
+  L.q_row = D;
+  L.q_head = (int64_t)S * D;
+  L.q_batch = (int64_t)Hq * S * D;
+  L.kv_row = D;
+  L.kv_head = (int64_t)S * D;
+  L.kv_batch = (int64_t)Hkv * S * D;
+  L.r_head = S;
+  L.r_batch = (int64_t)Hq * S;
+  return L;
+}
+
+Layout packed_layout(const int* cu, int nseq, int max_seqlen, int total, int Hq, int Hkv, int D) {
+  Layout L{};
+  L.cu = cu;
+  L.S = max_seqlen;
+  L.total = total;
+  L.nseg = nseq;
+  L.Hq = Hq;
+  L.Hkv = Hkv;
+  L.group = Hq / Hkv;
+  L.q_row = (int64_t)Hq * D;
+  L.q_head = D;
+  L.q_batch = 0;
+  L.kv_row = (int64_t)Hkv * D;
+  L.kv_head = D;
+  L.kv_batch = 0;
+  L.r_head = total;
+  L.r_batch = 0;
+  return L;
+}
+
+bool any_null(std::initializer_list<const void*> ps) {
+  for (const void* p : ps)
+    if (!p) return true;
+  return false;
+}
+
+bool any_misaligned(std::initializer_list<const void*> ps) {
+  for (const void* p : ps)
+    if (misaligned(p)) return true;
+  return false;
+}
+
+int fwd_common(const void* q, const void* k, const void* v, void* o, float* lse,
+               const Layout& L, int D, int causal, float scale, hipStream_t stream) {
+  if (any_null({q, k, v, o, lse})) return ATTN_ERR_NULL;
+  if (any_misaligned({q, k, v, o, lse})) return ATTN_ERR_ALIGN;
+  attn::FwdArgs a;
+  a.L = L;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.o = static_cast<uint16_t*>(o);
+  a.lse = lse;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.causal = causal;
+  return attn::launch_fwd(a, D, stream) == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
+}
+
+int bwd_common(const void* q, const void* k, const void* v, const void* o, const float* lse,
+               const void* dO, void* dq, void* dk, void* dv, const Layout& L, int D, int causal,
+               float scale, void* ws, size_t ws_bytes, size_t ws_need, int phases,
+               hipStream_t stream) {
+  if (phases < 1 || phases > 3) return ATTN_ERR_VALUE;
+  if (any_null({q, k, v, o, lse, dO, dq, dk, dv})) return ATTN_ERR_NULL;
+  if (any_misaligned({q, k, v, o, lse, dO, dq, dk, dv})) return ATTN_ERR_ALIGN;
+  if (!ws || ws_bytes < ws_need) return ATTN_ERR_WORKSPACE;
+  if (misaligned(ws)) return ATTN_ERR_ALIGN;
+  attn::BwdArgs a;
+  a.L = L;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.o = static_cast<const uint16_t*>(o);
+  a.lse = lse;
+  a.dout = static_cast<const uint16_t*>(dO);
+  a.dq = static_cast<uint16_t*>(dq);
+  a.dk = static_cast<uint16_t*>(dk);
+  a.dv = static_cast<uint16_t*>(dv);
+  a.delta = static_cast<float*>(ws);
+  a.scale = scale;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.causal = causal;
+  return attn::launch_bwd(a, D, phases, stream) == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
+}
+
+size_t delta_bytes(int64_t rows_times_heads) {
+  // fp32 Delta per (row, query head), rounded up to 256 bytes.
+  return (size_t)((rows_times_heads * 4 + 255) / 256 * 256);
+}
+
+}  // namespace
+
+extern "C" {
+
+int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
+             int Hkv, int S, int D, int causal, float scale, hipStream_t stream) {
+  int st = check_common(Hq, Hkv, D, causal, scale);
+  if (st != ATTN_OK) return st;
+  if (B < 0 || (st = check_rows(S)) != ATTN_OK) return ATTN_ERR_SHAPE;
+  if ((int64_t)B * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
+  if (B == 0 || S == 0) return ATTN_OK;
+  return fwd_common(q, k, v, o, lse, fixed_layout(B, Hq, Hkv, S, D), D, causal, scale, stream);
+}
+
+size_t attn_bwd_workspace_size(int B, int Hq, int Hkv, int S, int D) {
+  (void)Hkv;
+  (void)D;
+  if (B <= 0 || Hq <= 0 || S <= 0) return 0;
+  return delta_bytes((int64_t)B * Hq * S);
+}
+
+int attn_bwd_phases(const void* q, const void* k, const void* v, const void* o, const float* lse,
+                    const void* dO, void* dq, void* dk, void* dv, int B, int Hq, int Hkv, int S,
+                    int D, int causal, float scale, void* workspace, size_t workspace_bytes,
+                    int phases, hipStream_t stream) {
+  int st = check_common(Hq, Hkv, D, causal, scale);
+  if (st != ATTN_OK) return st;
+  if (B < 0 || check_rows(S) != ATTN_OK) return ATTN_ERR_SHAPE;
+  if ((int64_t)B * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
+  if (phases < 1 || phases > 3) return ATTN_ERR_VALUE;
+  if (B == 0 || S == 0) return ATTN_OK;
+  return bwd_common(q, k, v, o, lse, dO, dq, dk, dv, fixed_layout(B, Hq, Hkv, S, D), D, causal,
+                    scale, workspace, workspace_bytes, attn_bwd_workspace_size(B, Hq, Hkv, S, D),
+                    phases, stream);
+}
+
+int attn_bwd(const void* q, const void* k, const void* v, const void* o, const float* lse,
+             const void* dO, void* dq, void* dk, void* dv, int B, int Hq, int Hkv, int S, int D,
+             int causal, float scale, void* workspace, size_t workspace_bytes,
+             hipStream_t stream) {
+  return attn_bwd_phases(q, k, v, o, lse, dO, dq, dk, dv, B, Hq, Hkv, S, D, causal, scale,
+                         workspace, workspace_bytes, ATTN_BWD_DQ | ATTN_BWD_DKDV, stream);
+}
+
+int attn_fwd_varlen(const void* q, const void* k, const void* v, void* o, float* lse,
+                    const int* cu_seqlens, int nseq, int max_seqlen, int total, int Hq, int Hkv,
+                    int D, int causal, float scale, hipStream_t stream) {
+  int st = check_common(Hq, Hkv, D, causal, scale);
+  if (st != ATTN_OK) return st;
+  if (nseq < 0 || total < 0 || check_rows(max_seqlen) != ATTN_OK) return ATTN_ERR_SHAPE;
+  if ((int64_t)nseq * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
+  if (nseq == 0 || total == 0) return ATTN_OK;
+  if (max_seqlen < 1) return ATTN_ERR_VALUE;
+  if (!cu_seqlens) return ATTN_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(cu_seqlens) & 3u) return ATTN_ERR_ALIGN;
+  return fwd_common(q, k, v, o, lse, packed_layout(cu_seqlens, nseq, max_seqlen, total, Hq, Hkv, D),
+                    D, causal, scale, stream);
+}
+
+size_t attn_bwd_varlen_workspace_size(int total, int Hq, int Hkv, int D) {
+  (void)Hkv;
+  (void)D;
+  if (total <= 0 || Hq <= 0) return 0;
+  return delta_bytes((int64_t)total * Hq);
+}
+
+int attn_bwd_varlen_phases(const void* q, const void* k, const void* v, const void* o,
+                           const float* lse, const void* dO, void* dq, void* dk, void* dv,
+                           const int* cu_seqlens, int nseq, int max_seqlen, int total, int Hq,
+                           int Hkv, int D, int causal, float scale, void* workspace,
+                           size_t workspace_bytes, int phases, hipStream_t stream) {
+  int st = check_common(Hq, Hkv, D, causal, scale);
+  if (st != ATTN_OK) return st;
+  if (nseq < 0 || total < 0 || check_rows(max_seqlen) != ATTN_OK) return ATTN_ERR_SHAPE;
+  if ((int64_t)nseq * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
+  if (phases < 1 || phases > 3) return ATTN_ERR_VALUE;
+  if (nseq == 0 || total == 0) return ATTN_OK;
+  if (max_seqlen < 1) return ATTN_ERR_VALUE;
+  if (!cu_seqlens) return ATTN_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(cu_seqlens) & 3u) return ATTN_ERR_ALIGN;
+  return bwd_common(q, k, v, o, lse, dO, dq, dk, dv,
+                    packed_layout(cu_seqlens, nseq, max_seqlen, total, Hq, Hkv, D), D, causal,
+                    scale, workspace, workspace_bytes,
+                    attn_bwd_varlen_workspace_size(total, Hq, Hkv, D), phases, stream);
+}
+
+int attn_bwd_varlen(const void* q, const void* k, const void* v, const void* o, const float* lse,
+                    const void* dO, void* dq, void* dk, void* dv, const int* cu_seqlens, int nseq,
+                    int max_seqlen, int total, int Hq, int Hkv, int D, int causal, float scale,
+                    void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return attn_bwd_varlen_phases(q, k, v, o, lse, dO, dq, dk, dv, cu_seqlens, nseq, max_seqlen,
+                                total, Hq, Hkv, D, causal, scale, workspace, workspace_bytes,
+                                ATTN_BWD_DQ | ATTN_BWD_DKDV, stream);
+}
+
+const char* attn_status_string(int status) {
+  switch (status) {
+    case ATTN_OK: return "ok";
+    case ATTN_ERR_NULL: return "a required pointer is null";
+    case ATTN_ERR_SHAPE: return "a size is negative, a head count is below 1, or a size is too large";
+    case ATTN_ERR_GQA: return "Hq is not a multiple of Hkv";
+    case ATTN_ERR_HEAD_DIM: return "head dimension must be 64 or 128";
+    case ATTN_ERR_ALIGN: return "a pointer is not 16-byte aligned";
+    case ATTN_ERR_WORKSPACE: return "workspace is null or smaller than attn_bwd_workspace_size()";
+    case ATTN_ERR_HIP: return "a kernel launch failed";
+    case ATTN_ERR_VALUE:
+      return "scale is not finite, causal is not 0 or 1, max_seqlen < 1, or a bad phase mask";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,103 @@
+// Device-side building blocks shared by the attention kernels (gfx950).
+//
+// MFMA v_mfma_f32_32x32x16_bf16 operand conventions used throughout:
+//   A (32 x 16): lane l holds row (l % 32), reduction slots k = 8*(l/32) + e
+//                for its 8 bf16 elements e = 0..7;
+//   B (16 x 32): lane l holds column (l % 32), the same reduction slots;
+//   C (32 x 32): lane l holds column (l % 32) and, in accumulator element r,
+//                row 8*(r/4) + 4*(l/32) + (r%4).
+// Only the row/column placement and the identical slot assignment of A and B
+// matter: any consistent relabelling of the reduction index gives the same
+// sum, which is how accumulator tiles are fed back as B operands without a
+// shuffle through LDS.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace attn {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+      __builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// Two fp32 -> packed bf16 pair (round to nearest even; v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  bf16x2 v;
+  v[0] = (__bf16)lo;
+  v[1] = (__bf16)hi;
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Accumulator elements 8*c .. 8*c+7 of a 32x32 tile as a bf16 B operand.
+__device__ __forceinline__ u32x4 pack_chunk(const f32x16& x, int c) {
+  u32x4 r;
+  r[0] = pack_bf16(x[8 * c + 0], x[8 * c + 1]);
+  r[1] = pack_bf16(x[8 * c + 2], x[8 * c + 3]);
+  r[2] = pack_bf16(x[8 * c + 4], x[8 * c + 5]);
+  r[3] = pack_bf16(x[8 * c + 6], x[8 * c + 7]);
+  return r;
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Value of the partner lane l ^ 32 (the other half of the wavefront).
+__device__ __forceinline__ float swap_halves(float x) { return __shfl_xor(x, 32); }
+
+__device__ __forceinline__ u32x4 ld16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ u32x2 ld8(const uint16_t* p) { return *reinterpret_cast<const u32x2*>(p); }
+__device__ __forceinline__ void st16(uint16_t* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+__device__ __forceinline__ void st8(uint16_t* p, u32x2 v) { *reinterpret_cast<u32x2*>(p) = v; }
+
+// 4 rows x 8 bf16 (one u32x4 per row) -> 8 columns x 4 bf16 (one u32x2 per
+// column): out[c] = {row0[c], row1[c], row2[c], row3[c]}.
+__device__ __forceinline__ void transpose4x8(const u32x4 (&in)[4], u32x2 (&out)[8]) {
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    out[2 * m][0] = (in[0][m] & 0xffffu) | (in[1][m] << 16);
+    out[2 * m][1] = (in[2][m] & 0xffffu) | (in[3][m] << 16);
+    out[2 * m + 1][0] = (in[0][m] >> 16) | (in[1][m] & 0xffff0000u);
+    out[2 * m + 1][1] = (in[2][m] >> 16) | (in[3][m] & 0xffff0000u);
+  }
+}
+
+// Resolve segment z of a layout: first row offset (elements) and length.
+// Packed offsets are clamped into [0, total] so a malformed cu_seqlens array
+// cannot move any access outside the tensors.
+struct Segment {
+  int start;   // first row (packed) or 0
+  int len;     // rows in this segment
+};
+
+template <typename LayoutT>
+__device__ __forceinline__ Segment segment_of(const LayoutT& L, int z) {
+  Segment s;
+  if (L.cu) {
+    int a = L.cu[z], b = L.cu[z + 1];
+    a = a < 0 ? 0 : (a > L.total ? L.total : a);
+    b = b < a ? a : (b > L.total ? L.total : b);
+    s.start = a;
+    s.len = b - a;
+    if (s.len > L.S) s.len = L.S;
+  } else {
+    s.start = 0;
+    s.len = L.S;
+  }
+  return s;
+}
+
+}  // namespace attn

@@ -1,0 +1,143 @@
+"""Host-only tests of the C ABI: the library loads, exports every symbol of
+include/attn.h, and rejects every invalid argument with its status code
+before any GPU call (pointers here are fake integers; they are never
+dereferenced because validation fails first)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_17379_amd import attn
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+A = 0x10000   # a fake, 16-byte aligned "device address"
+
+
+def header_symbols():
+    text = open(os.path.join(ROOT, "include", "attn.h")).read()
+    return set(re.findall(r"^\s*(?:int|size_t|const char\*)\s+(attn_\w+)\s*\(", text, re.M))
+
+
+def test_phase_mask_validation():
+    l = attn.lib()
+    args = [A] * 9 + [1, 2, 2, 64, 64, 1, 0.125, A, 1 << 20]
+    for bad in (0, 4, -1):
+        assert l.attn_bwd_phases(*args, bad, None) == -8
+    argsv = [A] * 10 + [2, 64, 100, 2, 1, 128, 1, 0.1, A, 1 << 20]
+    for bad in (0, 4):
+        assert l.attn_bwd_varlen_phases(*argsv, bad, None) == -8
+    assert l.attn_bwd_phases(*(args[:-2] + [A, 1]), 2, None) == -6
+
+
+def test_library_exports_every_declared_symbol():
+    syms = header_symbols()
+    assert syms == set(attn.EXPORTS)
+    l = attn.lib()
+    for s in syms:
+        assert hasattr(l, s), s
+
+
+def fwd(**kw):
+    args = dict(q=A, k=A, v=A, o=A, lse=A, B=1, Hq=2, Hkv=2, S=64, D=64, causal=0, scale=0.125)
+    args.update(kw)
+    return attn.lib().attn_fwd(args["q"], args["k"], args["v"], args["o"], args["lse"], args["B"],
+                               args["Hq"], args["Hkv"], args["S"], args["D"], args["causal"],
+                               args["scale"], None)
+
+
+def bwd(**kw):
+    args = dict(q=A, k=A, v=A, o=A, lse=A, dO=A, dq=A, dk=A, dv=A, B=1, Hq=2, Hkv=2, S=64, D=64,
+                causal=1, scale=0.125, ws=A, wsb=1 << 20)
+    args.update(kw)
+    return attn.lib().attn_bwd(*(args[n] for n in ("q", "k", "v", "o", "lse", "dO", "dq", "dk",
+                                                    "dv", "B", "Hq", "Hkv", "S", "D", "causal",
+                                                    "scale", "ws", "wsb")), None)
+
+
+def fwdv(**kw):
+    args = dict(q=A, k=A, v=A, o=A, lse=A, cu=A, nseq=2, ms=64, T=100, Hq=2, Hkv=1, D=128,
+                causal=1, scale=0.1)
+    args.update(kw)
+    return attn.lib().attn_fwd_varlen(*(args[n] for n in ("q", "k", "v", "o", "lse", "cu", "nseq",
+                                                           "ms", "T", "Hq", "Hkv", "D", "causal",
+                                                           "scale")), None)
+
+
+def bwdv(**kw):
+    args = dict(q=A, k=A, v=A, o=A, lse=A, dO=A, dq=A, dk=A, dv=A, cu=A, nseq=2, ms=64, T=100,
+                Hq=2, Hkv=1, D=128, causal=1, scale=0.1, ws=A, wsb=1 << 20)
+    args.update(kw)
+    return attn.lib().attn_bwd_varlen(*(args[n] for n in (
+        "q", "k", "v", "o", "lse", "dO", "dq", "dk", "dv", "cu", "nseq", "ms", "T", "Hq", "Hkv",
+        "D", "causal", "scale", "ws", "wsb")), None)
+
+
+@pytest.mark.parametrize("call", [fwd, bwd, fwdv, bwdv])
+def test_scalar_validation(call):
+    assert call(Hq=0) == -2
+    assert call(Hkv=0) == -2
+    assert call(Hq=3, Hkv=2) == -3
+    assert call(D=96) == -4
+    assert call(D=256) == -4
+    assert call(causal=2) == -8
+    assert call(scale=float("nan")) == -8
+    assert call(scale=float("inf")) == -8
+    assert call(q=0) == -1
+    assert call(k=A + 8) == -5
+    assert call(lse=A + 4) == -5
+
+
+@pytest.mark.parametrize("call", [fwd, bwd])
+def test_fixed_shape_validation(call):
+    assert call(B=-1) == -2
+    assert call(S=-5) == -2
+    assert call(S=65535 * 128 + 1) == -2
+    # empty problems are no-ops and may carry null pointers
+    assert call(B=0, q=0, k=0, v=0, o=0, lse=0) == 0
+    assert call(S=0, q=0, k=0, v=0, o=0, lse=0) == 0
+
+
+@pytest.mark.parametrize("call", [fwdv, bwdv])
+def test_packed_shape_validation(call):
+    assert call(nseq=-1) == -2
+    assert call(T=-1) == -2
+    assert call(ms=0) == -8
+    assert call(cu=0) == -1
+    assert call(cu=A + 2) == -5
+    assert call(nseq=0, q=0, cu=0) == 0
+    assert call(T=0, q=0, cu=0) == 0
+
+
+def test_workspace_validation():
+    need = attn.attn_bwd_workspace_size(1, 2, 2, 64, 64)
+    assert need >= 1 * 2 * 64 * 4 and need % 256 == 0
+    assert bwd(wsb=need - 1) == -6
+    assert bwd(ws=0) == -6
+    assert bwd(ws=A + 8) == -5
+    needv = attn.attn_bwd_varlen_workspace_size(100, 2, 1, 128)
+    assert needv >= 100 * 2 * 4
+    assert bwdv(wsb=needv - 1) == -6
+    assert attn.attn_bwd_workspace_size(0, 2, 2, 64, 64) == 0
+
+
+def test_status_strings():
+    for code in range(-8, 1):
+        s = attn.attn_status_string(code)
+        assert s and s != "unknown status"
+    assert attn.attn_status_string(-99) == "unknown status"
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    q = torch.zeros(1, 1, 4, 64, dtype=torch.bfloat16)
+    lse = torch.zeros(1, 1, 4)
+    with pytest.raises(ValueError):
+        attn.attn_fwd(q, q, q, q.clone(), lse, False, 0.125)
+
+
+def test_cu_seqlens_host_check():
+    attn.check_cu_seqlens([0, 3, 3, 10], 10, 7)
+    for bad, total, ms in (([1, 3], 3, 5), ([0, 4, 3], 3, 5), ([0, 3], 4, 5), ([0, 9], 9, 5)):
+        with pytest.raises(ValueError):
+            attn.check_cu_seqlens(bad, total, ms)

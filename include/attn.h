@@ -59,20 +59,21 @@ extern "C" {
 typedef enum {
   ATTN_OK = 0,
   ATTN_ERR_NULL = -1,       /* a required pointer is null */
-  ATTN_ERR_SHAPE = -2,      /* a size is negative, Hq/Hkv < 1, or too large */
+  ATTN_ERR_SHAPE = -2,      /* a size is negative, Hq/Hkv < 1, or too large
+                               (S or max_seqlen > 65535*128, Hq*D > 2^22) */
   ATTN_ERR_GQA = -3,        /* Hq is not a multiple of Hkv */
   ATTN_ERR_HEAD_DIM = -4,   /* D is not 64 or 128 */
   ATTN_ERR_ALIGN = -5,      /* a pointer is not 16-byte aligned */
   ATTN_ERR_WORKSPACE = -6,  /* workspace null or smaller than required */
   ATTN_ERR_HIP = -7,        /* a kernel launch failed (hipGetLastError) */
-  ATTN_ERR_VALUE = -8       /* scale not finite, causal not 0/1, max_seqlen < 1,
-                               or a bad backward phase mask */
+  ATTN_ERR_VALUE = -8       /* scale not finite or not > 0, causal not 0/1,
+                               max_seqlen < 1, or a bad backward phase mask */
 } attn_status_t;
 
 /*
  * Forward, fixed length.  q [B,Hq,S,D], k/v [B,Hkv,S,D] in; o [B,Hq,S,D] and
- * lse [B,Hq,S] out.  causal is 0 or 1; scale is the softmax scale (1/sqrt(D)
- * in every measured workload).
+ * lse [B,Hq,S] out.  causal is 0 or 1; scale is the softmax scale, finite
+ * and > 0 (1/sqrt(D) in every measured workload).
  */
 int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
              int B, int Hq, int Hkv, int S, int D, int causal, float scale,

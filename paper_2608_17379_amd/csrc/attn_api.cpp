@@ -21,8 +21,12 @@ int check_common(int Hq, int Hkv, int D, int causal, float scale) {
   if (Hq < 1 || Hkv < 1) return ATTN_ERR_SHAPE;
   if (Hq % Hkv != 0) return ATTN_ERR_GQA;
   if (D != 64 && D != 128) return ATTN_ERR_HEAD_DIM;
+  // Bytes of 128 rows of one packed tensor must fit the 31-bit offsets of
+  // the kernels' buffer loads.
+  if ((int64_t)Hq * D * 2 * 128 > 0x7fffffff) return ATTN_ERR_SHAPE;
   if (causal != 0 && causal != 1) return ATTN_ERR_VALUE;
-  if (!isfinite(scale)) return ATTN_ERR_VALUE;
+  // The kernels take row maxima of the raw scores, so the scale must be > 0.
+  if (!(scale > 0.f) || !isfinite(scale)) return ATTN_ERR_VALUE;
   return ATTN_OK;
 }
 
@@ -238,7 +242,8 @@ const char* attn_status_string(int status) {
     case ATTN_ERR_WORKSPACE: return "workspace is null or smaller than attn_bwd_workspace_size()";
     case ATTN_ERR_HIP: return "a kernel launch failed";
     case ATTN_ERR_VALUE:
-      return "scale is not finite, causal is not 0 or 1, max_seqlen < 1, or a bad phase mask";
+      return "scale is not finite and > 0, causal is not 0 or 1, max_seqlen < 1, or a bad phase "
+             "mask";
     default: return "unknown status";
   }
 }

@@ -31,6 +31,41 @@ namespace {
 
 constexpr int kThreads = 256;
 
+// Read offsets of this lane into a swizzled row-major [64][D] LDS tile for an
+// MFMA operand over rows 32*b + (lane % 32): element offset of the 16-byte
+// chunk 2c + half.  The swizzle does not depend on row bit 5, so the two
+// 32-row blocks differ by a constant.
+template <int D>
+struct RowTileReader {
+  int off[D / 16];
+  __device__ __forceinline__ RowTileReader(int l32, int half) {
+    const int x = swz_row<D>(l32);
+#pragma unroll
+    for (int c = 0; c < D / 16; ++c) off[c] = l32 * D + 8 * ((2 * c + half) ^ x);
+  }
+  __device__ __forceinline__ int at(int b, int c) const { return off[c] + 32 * b * D; }
+};
+
+// Store a 4-row x 8-column block (rows 4*rg .. 4*rg+3, column chunk cc) into
+// a swizzled row-major [64][D] tile and, optionally, a transposed [D][kTS]
+// tile.
+template <int D>
+__device__ __forceinline__ void store_block(uint16_t* rowtile, uint16_t* ttile, const BlockMap<D>& m,
+                                            const u32x4 (&blk)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int j = store_row_order<D>(i, m.cc);
+    const int r = 4 * m.rg + j;
+    st16(&rowtile[r * D + 8 * (m.cc ^ swz_row<D>(r))], blk[j]);
+  }
+  if (ttile) {
+    u32x2 cols[8];
+    transpose4x8(blk, cols);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) st8(&ttile[(8 * m.cc + e) * kTS + 4 * m.rg], cols[e]);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // dQ (and Delta)
 // ---------------------------------------------------------------------------
@@ -38,23 +73,13 @@ constexpr int kQM = 128;   // query rows per workgroup
 constexpr int kQN = 64;    // keys per iteration
 
 template <int D>
-struct DqTile {
-  static constexpr int RS = D + 8;        // row-major tile stride, bf16
-  static constexpr int TS = kQN + 4;      // transposed tile stride, bf16
-  static constexpr int CPR = D / 8;
-  static constexpr int BLK = (kQN / 4) * CPR;   // 4-row x 8-col blocks per tile
-  static_assert(BLK <= kThreads, "tile split");
-};
-
-template <int D>
 __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(BwdArgs a) {
-  using T = DqTile<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t sk[kQN * T::RS];
-  __shared__ __attribute__((aligned(16))) uint16_t skt[D * T::TS];
-  __shared__ __attribute__((aligned(16))) uint16_t sv[kQN * T::RS];
+  __shared__ __attribute__((aligned(16))) uint16_t sk[kQN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t skt[D * kTS];
+  __shared__ __attribute__((aligned(16))) uint16_t sv[kQN * D];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = wave_id();
   const int l32 = lane & 31, half = lane >> 5;
 
   const Layout& L = a.L;
@@ -73,6 +98,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(BwdArgs a) {
                        (int64_t)h * L.r_head;
   const uint16_t* kp = a.k + kvoff;
   const uint16_t* vp = a.v + kvoff;
+  const int kvrow_b = (int)(L.kv_row * 2);
 
   const int qw0 = q0 + wave * 32;
   const int qrow = qw0 + l32;
@@ -81,16 +107,20 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(BwdArgs a) {
   // Q^T and dO^T as B operands; Delta from dO and O in the same layout.
   u32x4 qreg[D / 16], doreg[D / 16];
   float dsum = 0.f;
+  {
+    const rsrc_t rq = rows_rsrc(a.q + qoff, qw0, seg.len, L.q_row);
+    const rsrc_t rdo = rows_rsrc(a.dout + qoff, qw0, seg.len, L.q_row);
+    const rsrc_t ro = rows_rsrc(a.o + qoff, qw0, seg.len, L.q_row);
+    const int base = l32 * (int)(L.q_row * 2) + 16 * half;
 #pragma unroll
-  for (int c = 0; c < D / 16; ++c) {
-    const int64_t off = qoff + (int64_t)qrow * L.q_row + 16 * c + 8 * half;
-    const u32x4 z4 = {0u, 0u, 0u, 0u};
-    qreg[c] = valid ? ld16(a.q + off) : z4;
-    doreg[c] = valid ? ld16(a.dout + off) : z4;
-    const u32x4 ov = valid ? ld16(a.o + off) : z4;
+    for (int c = 0; c < D / 16; ++c) {
+      qreg[c] = bload16(rq, base + 32 * c);
+      doreg[c] = bload16(rdo, base + 32 * c);
+      const u32x4 ov = bload16(ro, base + 32 * c);
 #pragma unroll
-    for (int w = 0; w < 4; ++w)
-      dsum += bf16_lo(doreg[c][w]) * bf16_lo(ov[w]) + bf16_hi(doreg[c][w]) * bf16_hi(ov[w]);
+      for (int w = 0; w < 4; ++w)
+        dsum += bf16_lo(doreg[c][w]) * bf16_lo(ov[w]) + bf16_hi(doreg[c][w]) * bf16_hi(ov[w]);
+    }
   }
   const float delta = dsum + swap_halves(dsum);
   float lse2 = INFINITY;   // exp2(s*scale*log2e - lse2) = 0 for rows outside
@@ -103,41 +133,36 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(BwdArgs a) {
   const int kend = a.causal ? min(seg.len, q0 + kQM) : seg.len;
   const int nkt = (kend + kQN - 1) / kQN;
 
-  // Staging: K as a 4-row x 8-col block (stored both row-major and
-  // transposed), V as a 4-row x 8-col block stored row-major.
+  // Staging: K and V as 4-row x 8-column blocks.
+  const BlockMap<D> bm(tid);
   u32x4 kst[4], vst[4];
-  const int bkg = tid / T::CPR, bdc = tid % T::CPR;
-  const bool loader = tid < T::BLK;
   auto gload = [&](int kt) {
-    if (!loader) return;
+    if (!bm.active) return;
     const int k0 = kt * kQN;
+    const rsrc_t rk = rows_rsrc(kp, k0, seg.len, L.kv_row);
+    const rsrc_t rv = rows_rsrc(vp, k0, seg.len, L.kv_row);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int key = k0 + 4 * bkg + i;
-      const bool in = key < seg.len;
-      const int64_t off = (int64_t)key * L.kv_row + 8 * bdc;
-      kst[i] = in ? ld16(kp + off) : u32x4{0u, 0u, 0u, 0u};
-      vst[i] = in ? ld16(vp + off) : u32x4{0u, 0u, 0u, 0u};
+      const int off = (4 * bm.rg + i) * kvrow_b + 16 * bm.cc;
+      kst[i] = bload16(rk, off);
+      vst[i] = bload16(rv, off);
     }
   };
   auto sstore = [&]() {
-    if (!loader) return;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      st16(&sk[(4 * bkg + i) * T::RS + 8 * bdc], kst[i]);
-      st16(&sv[(4 * bkg + i) * T::RS + 8 * bdc], vst[i]);
-    }
-    u32x2 cols[8];
-    transpose4x8(kst, cols);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) st8(&skt[(8 * bdc + e) * T::TS + 4 * bkg], cols[e]);
+    if (!bm.active) return;
+    store_block<D>(sk, skt, bm, kst);
+    store_block<D>(sv, nullptr, bm, vst);
   };
+
+  const RowTileReader<D> rd(l32, half);
+  const uint16_t* ktrd = &skt[l32 * kTS + 4 * half];
 
   f32x16 dqacc[D / 32];
 #pragma unroll
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) dqacc[db][r] = 0.f;
+  const float sl2 = a.scale_log2;
 
   gload(0);
   sstore();
@@ -158,19 +183,19 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(BwdArgs a) {
       for (int c = 0; c < D / 16; ++c)
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
-          const int ro = (32 * kb + l32) * T::RS + 16 * c + 8 * half;
-          s[kb] = mfma32(ld16(&sk[ro]), qreg[c], s[kb]);
-          dp[kb] = mfma32(ld16(&sv[ro]), doreg[c], dp[kb]);
+          const int o = rd.at(kb, c);
+          s[kb] = mfma32(ld16(&sk[o]), qreg[c], s[kb]);
+          dp[kb] = mfma32(ld16(&sv[o]), doreg[c], dp[kb]);
         }
       const bool need_mask = (a.causal && k0 + kQN - 1 > qw0) || (k0 + kQN > seg.len);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float p = fast_exp2(s[kb][r] * a.scale_log2 - lse2);
+          float p = fast_exp2(__builtin_fmaf(s[kb][r], sl2, -lse2));
           if (need_mask) {
             const int key = k0 + 32 * kb + 8 * (r / 4) + 4 * half + (r % 4);
-            if ((a.causal && key > qrow) || key >= seg.len) p = 0.f;
+            p = ((a.causal && key > qrow) || key >= seg.len) ? 0.f : p;
           }
           s[kb][r] = p * (dp[kb][r] - delta);   // dS^T
         }
@@ -180,7 +205,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(BwdArgs a) {
         const u32x4 b = pack_chunk(s[c >> 1], c & 1);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
-          const uint16_t* row = &skt[(32 * db + l32) * T::TS + 16 * c + 4 * half];
+          const uint16_t* row = ktrd + 32 * db * kTS + 16 * c;
           const u32x2 lo = ld8(row), hi = ld8(row + 8);
           dqacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, b, dqacc[db]);
         }
@@ -214,26 +239,16 @@ constexpr int kKN = 128;   // keys per workgroup
 constexpr int kKM = 64;    // query rows per iteration
 
 template <int D>
-struct DkvTile {
-  static constexpr int RS = D + 8;
-  static constexpr int TS = kKM + 4;
-  static constexpr int CPR = D / 8;
-  static constexpr int BLK = (kKM / 4) * CPR;
-  static_assert(BLK <= kThreads, "tile split");
-};
-
-template <int D>
 __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
-  using T = DkvTile<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t sq[kKM * T::RS];
-  __shared__ __attribute__((aligned(16))) uint16_t sqt[D * T::TS];
-  __shared__ __attribute__((aligned(16))) uint16_t sdo[kKM * T::RS];
-  __shared__ __attribute__((aligned(16))) uint16_t sdot[D * T::TS];
+  __shared__ __attribute__((aligned(16))) uint16_t sq[kKM * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sqt[D * kTS];
+  __shared__ __attribute__((aligned(16))) uint16_t sdo[kKM * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sdot[D * kTS];
   __shared__ __attribute__((aligned(16))) float slse[kKM];
   __shared__ __attribute__((aligned(16))) float sdelta[kKM];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = wave_id();
   const int l32 = lane & 31, half = lane >> 5;
 
   const Layout& L = a.L;
@@ -246,6 +261,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
                         (int64_t)hk * L.kv_head;
   const int64_t qseg = L.cu ? (int64_t)seg.start * L.q_row : (int64_t)z * L.q_batch;
   const int64_t rseg = L.cu ? (int64_t)seg.start : (int64_t)z * L.r_batch;
+  const int qrow_b = (int)(L.q_row * 2);
 
   const int kw0 = k0 + wave * 32;
   const int krow = kw0 + l32;
@@ -253,11 +269,15 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
 
   // K and V rows of this lane's key as B operands of S = Q K^T, dP = dO V^T.
   u32x4 kreg[D / 16], vreg[D / 16];
+  {
+    const rsrc_t rk = rows_rsrc(a.k + kvoff, kw0, seg.len, L.kv_row);
+    const rsrc_t rv = rows_rsrc(a.v + kvoff, kw0, seg.len, L.kv_row);
+    const int base = l32 * (int)(L.kv_row * 2) + 16 * half;
 #pragma unroll
-  for (int c = 0; c < D / 16; ++c) {
-    const int64_t off = kvoff + (int64_t)krow * L.kv_row + 16 * c + 8 * half;
-    kreg[c] = kvalid ? ld16(a.k + off) : u32x4{0u, 0u, 0u, 0u};
-    vreg[c] = kvalid ? ld16(a.v + off) : u32x4{0u, 0u, 0u, 0u};
+    for (int c = 0; c < D / 16; ++c) {
+      kreg[c] = bload16(rk, base + 32 * c);
+      vreg[c] = bload16(rv, base + 32 * c);
+    }
   }
 
   f32x16 dkacc[D / 32], dvacc[D / 32];
@@ -276,23 +296,22 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
   const int per_head = nqt - it0;
   const int niter = per_head * L.group;
 
+  const BlockMap<D> bm(tid);
   u32x4 qst[4], dost[4];
   float lst = INFINITY, dst = 0.f;
-  const int bkg = tid / T::CPR, bdc = tid % T::CPR;
-  const bool loader = tid < T::BLK;
   auto gload = [&](int n) {
     const int g = n / per_head;
     const int qb = (it0 + n % per_head) * kKM;
     const int h = hk * L.group + g;
     const int64_t qoff = qseg + (int64_t)h * L.q_head;
-    if (loader) {
+    if (bm.active) {
+      const rsrc_t rq = rows_rsrc(a.q + qoff, qb, seg.len, L.q_row);
+      const rsrc_t rdo = rows_rsrc(a.dout + qoff, qb, seg.len, L.q_row);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int q = qb + 4 * bkg + i;
-        const bool in = q < seg.len;
-        const int64_t off = qoff + (int64_t)q * L.q_row + 8 * bdc;
-        qst[i] = in ? ld16(a.q + off) : u32x4{0u, 0u, 0u, 0u};
-        dost[i] = in ? ld16(a.dout + off) : u32x4{0u, 0u, 0u, 0u};
+        const int off = (4 * bm.rg + i) * qrow_b + 16 * bm.cc;
+        qst[i] = bload16(rq, off);
+        dost[i] = bload16(rdo, off);
       }
     }
     if (tid < kKM) {
@@ -309,25 +328,19 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
     }
   };
   auto sstore = [&]() {
-    if (loader) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        st16(&sq[(4 * bkg + i) * T::RS + 8 * bdc], qst[i]);
-        st16(&sdo[(4 * bkg + i) * T::RS + 8 * bdc], dost[i]);
-      }
-      u32x2 cols[8];
-      transpose4x8(qst, cols);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) st8(&sqt[(8 * bdc + e) * T::TS + 4 * bkg], cols[e]);
-      transpose4x8(dost, cols);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) st8(&sdot[(8 * bdc + e) * T::TS + 4 * bkg], cols[e]);
+    if (bm.active) {
+      store_block<D>(sq, sqt, bm, qst);
+      store_block<D>(sdo, sdot, bm, dost);
     }
     if (tid < kKM) {
       slse[tid] = lst;
       sdelta[tid] = dst;
     }
   };
+
+  const RowTileReader<D> rd(l32, half);
+  const int trd = l32 * kTS + 4 * half;
+  const float sl2 = a.scale_log2;
 
   if (niter > 0) {
     gload(0);
@@ -350,9 +363,9 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
       }
 #pragma unroll
       for (int c = 0; c < D / 16; ++c) {
-        const int ro = (32 * sb + l32) * T::RS + 16 * c + 8 * half;
-        s = mfma32(ld16(&sq[ro]), kreg[c], s);
-        dp = mfma32(ld16(&sdo[ro]), vreg[c], dp);
+        const int o = rd.at(sb, c);
+        s = mfma32(ld16(&sq[o]), kreg[c], s);
+        dp = mfma32(ld16(&sdo[o]), vreg[c], dp);
       }
       // s[r], dp[r]: query qs0 + 8(r/4) + 4half + r%4, key krow.
       const bool need_mask = a.causal && qs0 < kw0 + 31;
@@ -363,8 +376,8 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int r = 4 * g + i;
-          float p = fast_exp2(s[r] * a.scale_log2 - l4[i]);
-          if (need_mask && krow > qs0 + 8 * g + 4 * half + i) p = 0.f;
+          float p = fast_exp2(__builtin_fmaf(s[r], sl2, -l4[i]));
+          if (need_mask) p = krow > qs0 + 8 * g + 4 * half + i ? 0.f : p;
           s[r] = p;
           dp[r] = p * (dp[r] - d4[i]);   // dS
         }
@@ -373,14 +386,14 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
         const u32x4 pb = pack_chunk(s, c);
-        const u32x4 db_ = pack_chunk(dp, c);
+        const u32x4 dsb = pack_chunk(dp, c);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
-          const int ro = (32 * db + l32) * T::TS + 32 * sb + 16 * c + 4 * half;
+          const int ro = trd + 32 * db * kTS + 32 * sb + 16 * c;
           const u32x2 dlo = ld8(&sdot[ro]), dhi = ld8(&sdot[ro + 8]);
           dvacc[db] = mfma32(u32x4{dlo[0], dlo[1], dhi[0], dhi[1]}, pb, dvacc[db]);
           const u32x2 qlo = ld8(&sqt[ro]), qhi = ld8(&sqt[ro + 8]);
-          dkacc[db] = mfma32(u32x4{qlo[0], qlo[1], qhi[0], qhi[1]}, db_, dkacc[db]);
+          dkacc[db] = mfma32(u32x4{qlo[0], qlo[1], qhi[0], qhi[1]}, dsb, dkacc[db]);
         }
       }
     }

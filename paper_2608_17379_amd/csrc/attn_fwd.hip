@@ -1,8 +1,8 @@
 // Fused attention forward for gfx950: O = softmax(scale Q K^T + mask) V and
 // the row log-sum-exp, with the online-softmax recurrence of the corrected
 // FlashAttention-3 Algorithm 2 (PTXBench, Appendix A): per query block keep
-// the running row maximum m and row sum l, rescale the output accumulator by
-// exp(m_old - m_new) whenever the maximum moves, and normalise by l in the
+// a running row maximum m and row sum l, rescale the output accumulator by
+// exp(m_old - m_new) when the maximum moves, and normalise by l in the
 // epilogue, where L = m + log l.
 //
 // Work split: one workgroup of 4 wavefronts per (segment, query head, 128
@@ -12,10 +12,16 @@
 // are in-lane reductions plus one exchange with lane l ^ 32.  P^T, rounded to
 // bf16, is then already laid out as the B operand of O^T += V^T P^T.
 //
+// The reference maximum used for P is only moved when a tile's row maximum
+// exceeds it by more than 2^8 (in exp2 units), so most tiles skip the
+// rescale of O and l.  This is exact: O and l always share one reference,
+// and entries of P stay below 2^8, far inside fp32 and bf16 range.
+//
 // K tiles are stored row-major in LDS (each lane reads 16 contiguous bytes of
 // one key row); V tiles are transposed on their way into LDS so that the A
-// operand V^T is read as two 8-byte pieces.  The next tile's global loads are
-// issued before the current tile's MFMAs and land in LDS after them.
+// operand V^T is read as two 8-byte pieces.  Loads go through buffer
+// resources bounded at the sequence end, which return zero past it; the next
+// tile's loads are issued before the current tile's MFMAs.
 #include "attn_kernels.hpp"
 #include "device_common.hpp"
 
@@ -25,27 +31,25 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kBM = 128;   // query rows per workgroup
 constexpr int kBN = 64;    // keys per iteration
+constexpr float kRescaleSlack = 8.0f;   // log2 of the largest P entry allowed
 
 template <int D>
 struct FwdTile {
   static constexpr int KS = D + 8;                  // K row stride, bf16 (16 B pad)
-  static constexpr int VS = kBN + 4;                // V^T row stride, bf16 (8 B pad)
   static constexpr int CPR = D / 8;                 // 16-byte chunks per row
   static constexpr int KPASS = kBN * CPR / kThreads;
   static constexpr int KROWS = kThreads / CPR;      // K rows per pass
-  static constexpr int VBLK = (kBN / 4) * CPR;      // 4-key x 8-d blocks of V
   static_assert(KPASS * KROWS == kBN, "K tile split");
-  static_assert(VBLK <= kThreads, "V tile split");
 };
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   using T = FwdTile<D>;
   __shared__ __attribute__((aligned(16))) uint16_t sk[kBN * T::KS];
-  __shared__ __attribute__((aligned(16))) uint16_t svt[D * T::VS];
+  __shared__ __attribute__((aligned(16))) uint16_t svt[D * kTS];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = wave_id();
   const int l32 = lane & 31, half = lane >> 5;
 
   const Layout& L = a.L;
@@ -64,48 +68,49 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
                        (int64_t)h * L.r_head;
   const uint16_t* kp = a.k + kvoff;
   const uint16_t* vp = a.v + kvoff;
+  const int kvrow_b = (int)(L.kv_row * 2);   // bytes between key rows
 
   // This lane's query row, held as B operands of S^T = K Q^T:
   // qreg[c] = Q[qrow][16c + 8*half .. +8].
   const int qw0 = q0 + wave * 32;
   const int qrow = qw0 + l32;
   u32x4 qreg[D / 16];
+  {
+    const rsrc_t rq = rows_rsrc(a.q + qoff, qw0, seg.len, L.q_row);
+    const int base = l32 * (int)(L.q_row * 2) + 16 * half;
 #pragma unroll
-  for (int c = 0; c < D / 16; ++c)
-    qreg[c] = qrow < seg.len ? ld16(a.q + qoff + (int64_t)qrow * L.q_row + 16 * c + 8 * half)
-                             : u32x4{0u, 0u, 0u, 0u};
+    for (int c = 0; c < D / 16; ++c) qreg[c] = bload16(rq, base + 32 * c);
+  }
 
   const int kend = a.causal ? min(seg.len, q0 + kBM) : seg.len;
   const int nkt = (kend + kBN - 1) / kBN;
 
-  // Staging registers for the next K / V tile.
+  // Staging registers for the next K / V tile.  K: KPASS rows per thread,
+  // one 16-byte chunk each.  V: one 4-key x 8-d block per thread.
+  const int krow_ld = tid / T::CPR, kch = tid % T::CPR;
+  const BlockMap<D> vb(tid);
   u32x4 kst[T::KPASS];
   u32x4 vst[4];
-  const int krow_ld = tid / T::CPR, kch = tid % T::CPR;   // K: row, chunk
-  const int vkg = tid / T::CPR, vdc = tid % T::CPR;       // V: key group, d chunk
   auto gload = [&](int kt) {
     const int k0 = kt * kBN;
+    const rsrc_t rk = rows_rsrc(kp, k0, seg.len, L.kv_row);
+    const rsrc_t rv = rows_rsrc(vp, k0, seg.len, L.kv_row);
 #pragma unroll
-    for (int p = 0; p < T::KPASS; ++p) {
-      const int key = k0 + p * T::KROWS + krow_ld;
-      kst[p] = key < seg.len ? ld16(kp + (int64_t)key * L.kv_row + 8 * kch) : u32x4{0u, 0u, 0u, 0u};
-    }
-    if (tid < T::VBLK) {
+    for (int p = 0; p < T::KPASS; ++p)
+      kst[p] = bload16(rk, (p * T::KROWS + krow_ld) * kvrow_b + 16 * kch);
+    if (vb.active) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = k0 + 4 * vkg + i;
-        vst[i] = key < seg.len ? ld16(vp + (int64_t)key * L.kv_row + 8 * vdc) : u32x4{0u, 0u, 0u, 0u};
-      }
+      for (int i = 0; i < 4; ++i) vst[i] = bload16(rv, (4 * vb.rg + i) * kvrow_b + 16 * vb.cc);
     }
   };
   auto sstore = [&]() {
 #pragma unroll
     for (int p = 0; p < T::KPASS; ++p) st16(&sk[(p * T::KROWS + krow_ld) * T::KS + 8 * kch], kst[p]);
-    if (tid < T::VBLK) {
+    if (vb.active) {
       u32x2 cols[8];
       transpose4x8(vst, cols);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) st8(&svt[(8 * vdc + e) * T::VS + 4 * vkg], cols[e]);
+      for (int e = 0; e < 8; ++e) st8(&svt[(8 * vb.cc + e) * kTS + 4 * vb.rg], cols[e]);
     }
   };
 
@@ -114,8 +119,12 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
-  float m = -INFINITY;   // running max of scale*log2(e)*s for query qrow
-  float lsum = 0.f;      // this lane's share of the running row sum
+  float mref = -INFINITY;   // reference max of scale*log2(e)*s for query qrow
+  float lsum = 0.f;         // this lane's share of the row sum, relative to mref
+  const float sl2 = a.scale_log2;
+
+  const uint16_t* krd = &sk[l32 * T::KS + 8 * half];
+  const uint16_t* vrd = &svt[l32 * kTS + 4 * half];
 
   gload(0);
   sstore();
@@ -135,55 +144,59 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
       for (int c = 0; c < D / 16; ++c)
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
-          s[kb] = mfma32(ld16(&sk[(32 * kb + l32) * T::KS + 16 * c + 8 * half]), qreg[c], s[kb]);
+          s[kb] = mfma32(ld16(krd + 32 * kb * T::KS + 16 * c), qreg[c], s[kb]);
 
-      // s[kb][r] is the score of key k0 + 32kb + 8(r/4) + 4half + r%4.
-      const bool need_mask = (a.causal && k0 + kBN - 1 > qw0) || (k0 + kBN > seg.len);
-      float mx = -INFINITY;
+      // s[kb][r] is the raw score of key k0 + 32kb + 8(r/4) + 4half + r%4.
+      if ((a.causal && k0 + kBN - 1 > qw0) || k0 + kBN > seg.len) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = k0 + 32 * kb + 8 * (r / 4) + 4 * half + (r % 4);
+            const bool masked = (a.causal && key > qrow) || key >= seg.len;
+            s[kb][r] = masked ? -INFINITY : s[kb][r];
+          }
+      }
+      float mx = s[0][0];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float t = s[kb][r] * a.scale_log2;
-          if (need_mask) {
-            const int key = k0 + 32 * kb + 8 * (r / 4) + 4 * half + (r % 4);
-            if ((a.causal && key > qrow) || key >= seg.len) t = -INFINITY;
-          }
-          s[kb][r] = t;
-          mx = fmaxf(mx, t);
-        }
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
       mx = fmaxf(mx, swap_halves(mx));
-      const float mnew = fmaxf(m, mx);
-      const float mref = mnew == -INFINITY ? 0.f : mnew;
-      const float alpha = fast_exp2(m - mref);
+      const float mt = mx * sl2;   // this tile's row max in exp2 units
+      if (__ballot(mt > mref + kRescaleSlack)) {
+        const float mnew = fmaxf(mref, mt);
+        const float alpha = fast_exp2(mref - mnew);   // 0 on the first visible tile
+        lsum *= alpha;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+        mref = mnew;
+      }
+      const float mneg = mref == -INFINITY ? 0.f : -mref;
       float rs = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = fast_exp2(s[kb][r] - mref);
+          const float p = fast_exp2(__builtin_fmaf(s[kb][r], sl2, mneg));
           s[kb][r] = p;
           rs += p;
         }
-      lsum = lsum * alpha + rs;
-      m = mnew;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+      lsum += rs;
 
       // O^T[d][q] += sum_key V^T[d][key] P^T[key][q]; chunk c = keys 16c..16c+15.
-      u32x4 pb[4];
 #pragma unroll
-      for (int c = 0; c < 4; ++c) pb[c] = pack_chunk(s[c >> 1], c & 1);
+      for (int c = 0; c < 4; ++c) {
+        const u32x4 pb = pack_chunk(s[c >> 1], c & 1);
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const uint16_t* row = &svt[(32 * db + l32) * T::VS + 16 * c + 4 * half];
+        for (int db = 0; db < D / 32; ++db) {
+          const uint16_t* row = vrd + 32 * db * kTS + 16 * c;
           const u32x2 lo = ld8(row), hi = ld8(row + 8);
-          oacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb[c], oacc[db]);
+          oacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb, oacc[db]);
         }
+      }
     }
     __syncthreads();
     if (kt + 1 < nkt) {
@@ -206,7 +219,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
         w[1] = pack_bf16(oacc[db][4 * g + 2] * inv, oacc[db][4 * g + 3] * inv);
         st8(op + 32 * db + 8 * g + 4 * half, w);
       }
-    if (half == 0) a.lse[roff + qrow] = lsum > 0.f ? (m + log2f(lsum)) * kLn2 : -INFINITY;
+    if (half == 0) a.lse[roff + qrow] = lsum > 0.f ? (mref + log2f(lsum)) * kLn2 : -INFINITY;
   }
 }
 

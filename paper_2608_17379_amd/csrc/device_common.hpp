@@ -75,6 +75,86 @@ __device__ __forceinline__ void transpose4x8(const u32x4 (&in)[4], u32x2 (&out)[
   }
 }
 
+// Wavefront index as a scalar (the compiler cannot prove threadIdx.x >> 6 is
+// uniform, and a uniform value keeps wave-level decisions as scalar branches).
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
+
+// ---------------------------------------------------------------------------
+// Buffer loads: a resource over [base, base + bytes) makes out-of-range
+// loads return zero in hardware, with no branch and no access.
+// ---------------------------------------------------------------------------
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kRsrcFlags = 0x00020000;   // raw buffer, 32-bit data format (gfx9 family)
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  const int64_t lim = bytes < 0 ? 0 : (bytes > 0x7fffffff ? 0x7fffffff : bytes);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)lim, kRsrcFlags);
+}
+
+__device__ __forceinline__ u32x4 bload16(rsrc_t r, int byte_off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
+}
+
+// Rows [row0, len) of one head as a buffer resource: loads of rows >= len
+// (the tile tail) return zero.  row_stride in elements.
+__device__ __forceinline__ rsrc_t rows_rsrc(const uint16_t* head_base, int row0, int len,
+                                             int64_t row_stride) {
+  return make_rsrc(head_base + (int64_t)row0 * row_stride,
+                   (int64_t)(len - row0) * row_stride * 2);
+}
+
+// ---------------------------------------------------------------------------
+// LDS tile layouts.  gfx950's LDS serves 64 banks x 4 bytes per cycle (a
+// 16-byte access 16 lanes at a time, an 8-byte access 32 lanes at a time);
+// the layouts below are also conflict-free under a 32-bank model.
+//
+// Row-major tile [64][D] filled by 4-row x 8-column blocks, rows unpadded:
+// the 16-byte chunk c of row r lives at chunk c ^ swz_row<D>(r).  The
+// swizzle is a GF(2)-linear map of the row bits chosen so that sixteen
+// consecutive rows at one chunk (MFMA operand reads) and the block stores of
+// sixteen lanes (8 row groups x 2 chunks) hit distinct banks; for D = 64 the
+// two chunks of a store phase also take rows of opposite parity (see
+// store_row_order).
+template <int D>
+__device__ __forceinline__ int swz_row(int r) {
+  if constexpr (D == 128)
+    return (r & 7) ^ (((r >> 3) & 1) * 9) ^ (((r >> 4) & 1) * 2);
+  else
+    return (r & 7) ^ ((r >> 3) & 3);
+}
+
+// Row (0..3) of its 4-row block that a thread stores at step i.
+template <int D>
+__device__ __forceinline__ int store_row_order(int i, int cc) {
+  if constexpr (D == 64)
+    return i ^ (cc & 1);
+  else
+    return i;
+}
+
+// Transposed tile [D][64] with rows padded to 68 bf16 (136 bytes): sixteen
+// consecutive rows at one column, and one row at sixteen 8-byte chunks, both
+// land on sixteen distinct bank pairs.
+constexpr int kTS = 68;
+
+// Thread -> 4x8 block assignment for a tile of 64 rows x D columns
+// (16 row groups x D/8 column chunks): within every 16 lanes, 8 row groups
+// x 2 column chunks, so that the transposed 8-byte stores of 16 lanes and
+// the row-major 16-byte stores of 8 lanes are free of bank conflicts, and a
+// global load instruction reads 128 contiguous bytes from each of 8 rows.
+template <int D>
+struct BlockMap {
+  static constexpr int CPR = D / 8;            // column chunks
+  static constexpr int NBLK = 16 * CPR;        // blocks per 64-row tile
+  int rg, cc;                                  // row group (rows 4rg..4rg+3), column chunk
+  bool active;
+  __device__ __forceinline__ explicit BlockMap(int tid) {
+    active = tid < NBLK;
+    rg = (tid & 7) + 8 * (tid / (8 * CPR));
+    cc = (tid >> 3) % CPR;
+  }
+};
+
 // Resolve segment z of a layout: first row offset (elements) and length.
 // Packed offsets are clamped into [0, total] so a malformed cu_seqlens array
 // cannot move any access outside the tensors.

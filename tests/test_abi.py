@@ -83,6 +83,9 @@ def test_scalar_validation(call):
     assert call(causal=2) == -8
     assert call(scale=float("nan")) == -8
     assert call(scale=float("inf")) == -8
+    assert call(scale=0.0) == -8
+    assert call(scale=-0.125) == -8
+    assert call(Hq=65536, Hkv=1, D=128) == -2
     assert call(q=0) == -1
     assert call(k=A + 8) == -5
     assert call(lse=A + 4) == -5

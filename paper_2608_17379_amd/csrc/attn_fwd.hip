@@ -17,11 +17,12 @@
 // rescale of O and l.  This is exact: O and l always share one reference,
 // and entries of P stay below 2^8, far inside fp32 and bf16 range.
 //
-// K tiles are stored row-major in LDS (each lane reads 16 contiguous bytes of
-// one key row); V tiles are transposed on their way into LDS so that the A
-// operand V^T is read as two 8-byte pieces.  Loads go through buffer
-// resources bounded at the sequence end, which return zero past it; the next
-// tile's loads are issued before the current tile's MFMAs.
+// K and V tiles go from global memory straight into a ring of LDS stages
+// (buffer_load ... lds, bounded at the sequence end so that rows past it read
+// as zero), issued a stage ahead, with one barrier per tile.  Both stay
+// row-major in LDS: K is read as 16-byte rows, and the A operand V^T comes
+// out of the V tile through the transposing read ds_read_b64_tr_b16, so no
+// register staging or transposing store is needed.
 #include "attn_kernels.hpp"
 #include "device_common.hpp"
 
@@ -33,20 +34,17 @@ constexpr int kBM = 128;   // query rows per workgroup
 constexpr int kBN = 64;    // keys per iteration
 constexpr float kRescaleSlack = 8.0f;   // log2 of the largest P entry allowed
 
-template <int D>
-struct FwdTile {
-  static constexpr int KS = D + 8;                  // K row stride, bf16 (16 B pad)
-  static constexpr int CPR = D / 8;                 // 16-byte chunks per row
-  static constexpr int KPASS = kBN * CPR / kThreads;
-  static constexpr int KROWS = kThreads / CPR;      // K rows per pass
-  static_assert(KPASS * KROWS == kBN, "K tile split");
-};
+// Two LDS stages (2 x 32 KiB at D = 128: two workgroups per CU), declared as
+// separate objects so that the compiler can tell a stage being filled by DMA
+// from the one being read and does not wait for the prefetch.
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
-  using T = FwdTile<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t sk[kBN * T::KS];
-  __shared__ __attribute__((aligned(16))) uint16_t svt[D * kTS];
+  using Tile = AsyncTile<D>;
+  __shared__ __attribute__((aligned(1024))) uint16_t sk0[Tile::ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t sk1[Tile::ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t sv0[Tile::ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t sv1[Tile::ELEMS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = wave_id();
@@ -68,7 +66,6 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
                        (int64_t)h * L.r_head;
   const uint16_t* kp = a.k + kvoff;
   const uint16_t* vp = a.v + kvoff;
-  const int kvrow_b = (int)(L.kv_row * 2);   // bytes between key rows
 
   // This lane's query row, held as B operands of S^T = K Q^T:
   // qreg[c] = Q[qrow][16c + 8*half .. +8].
@@ -85,34 +82,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   const int kend = a.causal ? min(seg.len, q0 + kBM) : seg.len;
   const int nkt = (kend + kBN - 1) / kBN;
 
-  // Staging registers for the next K / V tile.  K: KPASS rows per thread,
-  // one 16-byte chunk each.  V: one 4-key x 8-d block per thread.
-  const int krow_ld = tid / T::CPR, kch = tid % T::CPR;
-  const BlockMap<D> vb(tid);
-  u32x4 kst[T::KPASS];
-  u32x4 vst[4];
-  auto gload = [&](int kt) {
-    const int k0 = kt * kBN;
-    const rsrc_t rk = rows_rsrc(kp, k0, seg.len, L.kv_row);
-    const rsrc_t rv = rows_rsrc(vp, k0, seg.len, L.kv_row);
-#pragma unroll
-    for (int p = 0; p < T::KPASS; ++p)
-      kst[p] = bload16(rk, (p * T::KROWS + krow_ld) * kvrow_b + 16 * kch);
-    if (vb.active) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) vst[i] = bload16(rv, (4 * vb.rg + i) * kvrow_b + 16 * vb.cc);
-    }
-  };
-  auto sstore = [&]() {
-#pragma unroll
-    for (int p = 0; p < T::KPASS; ++p) st16(&sk[(p * T::KROWS + krow_ld) * T::KS + 8 * kch], kst[p]);
-    if (vb.active) {
-      u32x2 cols[8];
-      transpose4x8(vst, cols);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) st8(&svt[(8 * vb.cc + e) * kTS + 4 * vb.rg], cols[e]);
-    }
-  };
+  const Tile dma(wave, lane, (int)(L.kv_row * 2));
+  const RowReader<D> kr(l32, half);
+  const TransReader<D> vr(lane);
 
   f32x16 oacc[D / 32];
 #pragma unroll
@@ -123,86 +95,108 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   float lsum = 0.f;         // this lane's share of the row sum, relative to mref
   const float sl2 = a.scale_log2;
 
-  const uint16_t* krd = &sk[l32 * T::KS + 8 * half];
-  const uint16_t* vrd = &svt[l32 * kTS + 4 * half];
-
-  gload(0);
-  sstore();
-  __syncthreads();
-  for (int kt = 0; kt < nkt; ++kt) {
-    if (kt + 1 < nkt) gload(kt + 1);
+  auto compute = [&](int kt, const uint16_t* kt_lds, const uint16_t* vt_lds) {
     const int k0 = kt * kBN;
-    // A tile whose first key is after this wavefront's last query is fully
-    // masked for it and changes nothing.
-    if (!a.causal || k0 <= qw0 + 31) {
-      f32x16 s[2];
+    f32x16 s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+#pragma unroll
+    for (int c = 0; c < D / 16; ++c)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
-#pragma unroll
-      for (int c = 0; c < D / 16; ++c)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-          s[kb] = mfma32(ld16(krd + 32 * kb * T::KS + 16 * c), qreg[c], s[kb]);
+        s[kb] = mfma32(ld16(kt_lds + kr.rm[c] + 32 * kb * D), qreg[c], s[kb]);
 
-      // s[kb][r] is the raw score of key k0 + 32kb + 8(r/4) + 4half + r%4.
-      if ((a.causal && k0 + kBN - 1 > qw0) || k0 + kBN > seg.len) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = k0 + 32 * kb + 8 * (r / 4) + 4 * half + (r % 4);
-            const bool masked = (a.causal && key > qrow) || key >= seg.len;
-            s[kb][r] = masked ? -INFINITY : s[kb][r];
-          }
-      }
-      float mx = s[0][0];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-      mx = fmaxf(mx, swap_halves(mx));
-      const float mt = mx * sl2;   // this tile's row max in exp2 units
-      if (__ballot(mt > mref + kRescaleSlack)) {
-        const float mnew = fmaxf(mref, mt);
-        const float alpha = fast_exp2(mref - mnew);   // 0 on the first visible tile
-        lsum *= alpha;
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
-        mref = mnew;
-      }
-      const float mneg = mref == -INFINITY ? 0.f : -mref;
-      float rs = 0.f;
+    // s[kb][r] is the raw score of key k0 + 32kb + 8(r/4) + 4half + r%4.
+    if ((a.causal && k0 + kBN - 1 > qw0) || k0 + kBN > seg.len) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = fast_exp2(__builtin_fmaf(s[kb][r], sl2, mneg));
-          s[kb][r] = p;
-          rs += p;
+          const int key = k0 + 32 * kb + 8 * (r / 4) + 4 * half + (r % 4);
+          const bool masked = (a.causal && key > qrow) || key >= seg.len;
+          s[kb][r] = masked ? -INFINITY : s[kb][r];
         }
-      lsum += rs;
+    }
+    float mx = s[0][0];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
+    mx = fmaxf(mx, swap_halves(mx));
+    const float mt = mx * sl2;   // this tile's row max in exp2 units
+    if (__ballot(mt > mref + kRescaleSlack)) {
+      const float mnew = fmaxf(mref, mt);
+      const float alpha = fast_exp2(mref - mnew);   // 0 on the first visible tile
+      lsum *= alpha;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+      mref = mnew;
+    }
+    const float mneg = mref == -INFINITY ? 0.f : -mref;
+    float rs = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = fast_exp2(__builtin_fmaf(s[kb][r], sl2, mneg));
+        s[kb][r] = p;
+        rs += p;
+      }
+    lsum += rs;
 
-      // O^T[d][q] += sum_key V^T[d][key] P^T[key][q]; chunk c = keys 16c..16c+15.
+    // O^T[d][q] += sum_key V^T[d][key] P^T[key][q]; chunk c = keys 16c..16c+15,
+    // V^T read transposed out of the row-major V tile.
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const u32x4 pb = pack_chunk(s[c >> 1], c & 1);
+    for (int c = 0; c < 4; ++c) {
+      const u32x4 pb = pack_chunk(s[c >> 1], c & 1);
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          const uint16_t* row = vrd + 32 * db * kTS + 16 * c;
-          const u32x2 lo = ld8(row), hi = ld8(row + 8);
-          oacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb, oacc[db]);
-        }
+      for (int db = 0; db < D / 32; ++db) {
+        const u32x2 lo = ld_tr(vt_lds + vr.tr[db][0] + 16 * c * D);
+        const u32x2 hi = ld_tr(vt_lds + vr.tr[db][1] + 16 * c * D);
+        oacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb, oacc[db]);
       }
     }
+  };
+  // One tile: wait for its loads (this wavefront's, then everyone's through
+  // the barrier, which also frees the stage read one tile earlier), start the
+  // next tile's loads into that stage, then compute.
+  auto step = [&](int kt, bool work, const uint16_t* kc, const uint16_t* vc, uint16_t* kn,
+                  uint16_t* vn) {
+    wait_vm<0>();
     __syncthreads();
     if (kt + 1 < nkt) {
-      sstore();
-      __syncthreads();
+      dma.load(rows_rsrc(kp, (kt + 1) * kBN, seg.len, L.kv_row), kn, wave);
+      dma.load(rows_rsrc(vp, (kt + 1) * kBN, seg.len, L.kv_row), vn, wave);
     }
+    if (work) compute(kt, kc, vc);
+  };
+
+  // Tiles past this wavefront's last query are fully masked for it: the
+  // wavefront only joins their barriers and loads.
+  const int nkt_w = a.causal ? min(nkt, (qw0 + 31) / kBN + 1) : nkt;
+  if (nkt > 0) {
+    dma.load(rows_rsrc(kp, 0, seg.len, L.kv_row), sk0, wave);
+    dma.load(rows_rsrc(vp, 0, seg.len, L.kv_row), sv0, wave);
+  }
+  wait_vm<0>();   // Q rows and the first tile
+  int kt = 0;
+  for (; kt + 1 < nkt_w; kt += 2) {
+    step(kt, true, sk0, sv0, sk1, sv1);
+    step(kt + 1, true, sk1, sv1, sk0, sv0);
+  }
+  if (kt < nkt_w) {
+    step(kt, true, sk0, sv0, sk1, sv1);
+    ++kt;
+  }
+  for (; kt < nkt; ++kt) {
+    if (kt & 1)
+      step(kt, false, sk1, sv1, sk0, sv0);
+    else
+      step(kt, false, sk0, sv0, sk1, sv1);
   }
 
   // Epilogue: O = O / l, L = (m + log2 l) ln 2.

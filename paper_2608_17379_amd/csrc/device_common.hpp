@@ -155,6 +155,103 @@ struct BlockMap {
   }
 };
 
+// ---------------------------------------------------------------------------
+// Asynchronous tiles: [64 rows][D] bf16 tiles filled straight from global
+// memory into LDS (buffer_load ... lds) and read back either row-major
+// (16-byte MFMA operand rows) or transposed (ds_read_b64_tr_b16).
+//
+// A DMA load writes 16 bytes per lane to consecutive LDS addresses (lane L
+// of the wave at base + 16 L), so the layout is chosen by which source chunk
+// each lane fetches: LDS granule p holds row p / (D/8), logical 16-byte chunk
+// (p % (D/8)) ^ tile_swz<D>(row).  The swizzle makes both read patterns hit
+// 64 distinct banks per access phase: sixteen consecutive rows at one chunk
+// (row-major reads), and four consecutive rows x four chunks (transposed
+// reads).
+// ---------------------------------------------------------------------------
+#define ATTN_LDS __attribute__((address_space(3)))
+typedef __attribute__((ext_vector_type(4))) short s16x4;
+
+template <int D>
+__device__ __forceinline__ int tile_swz(int r) {
+  if constexpr (D == 128)
+    return ((r & 3) << 2) | ((r >> 2) & 3);
+  else
+    return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+}
+
+template <int D>
+struct AsyncTile {
+  static constexpr int CPR = D / 8;          // 16-byte chunks per row
+  static constexpr int NJ = CPR / 4;         // DMA instructions per wavefront (4 wavefronts)
+  static constexpr int ELEMS = 64 * D;       // bf16 elements per tile
+  int goff[NJ];                              // this lane's source byte offset per instruction
+  __device__ __forceinline__ AsyncTile(int wave, int lane, int row_bytes) {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int p = (wave * NJ + j) * 64 + lane;
+      const int row = p / CPR;
+      const int logical = (p % CPR) ^ tile_swz<D>(row);
+      goff[j] = row * row_bytes + 16 * logical;
+    }
+  }
+  // Enqueue this wavefront's share of a tile: rows [0, 64) of `src` into
+  // `dst` (the tile base in LDS).
+  __device__ __forceinline__ void load(rsrc_t src, uint16_t* dst, int wave) const {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          src, (ATTN_LDS void*)(dst + (wave * NJ + j) * 64 * 8), 16, goff[j], 0, 0, 0);
+  }
+};
+
+// Row-major read offsets (elements) of an MFMA operand over rows
+// 32*b + (lane % 32), 16-byte chunk 2c + half: rm[c] + 32*b*D.
+template <int D>
+struct RowReader {
+  int rm[D / 16];
+  __device__ __forceinline__ RowReader(int l32, int half) {
+    const int x = tile_swz<D>(l32);
+#pragma unroll
+    for (int c = 0; c < D / 16; ++c) rm[c] = l32 * D + 8 * ((2 * c + half) ^ x);
+  }
+};
+
+// Transposed reads: the A operand of a 32x32x16 MFMA whose row index is a
+// column of the tile (d) and whose reduction index runs over tile rows.  For
+// column block db and 16-row chunk c, lane (l32, half) receives rows
+// 16c + 8(e/4) + 4 half + e%4 (e = 0..7) of column 32 db + l32, as two
+// ds_read_b64_tr_b16 at tr[db][0] + 16 c D and tr[db][1] + 16 c D.
+// (Within each 16-lane group, transposed read lane i returns element i % 4
+// of the 8 bytes addressed by lanes 4e + i/4, e = 0..3.)
+template <int D>
+struct TransReader {
+  int tr[D / 32][2];
+  __device__ __forceinline__ TransReader(int lane) {
+    const int grp = lane >> 4, j = lane & 15;
+    const int g = grp & 1, h = grp >> 1, e = j >> 2, m = j & 3;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int row = 8 * hh + 4 * h + e;
+        const int phys = (4 * db + 2 * g + (m >> 1)) ^ tile_swz<D>(row);
+        tr[db][hh] = row * D + 8 * phys + 4 * (m & 1);
+      }
+  }
+};
+
+__device__ __forceinline__ u32x2 ld_tr(const uint16_t* p) {
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS s16x4*)(p)));
+}
+
+// Wait until at most N vector-memory operations of this wavefront are in
+// flight (expcnt and lgkmcnt unconstrained).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
 // Resolve segment z of a layout: first row offset (elements) and length.
 // Packed offsets are clamped into [0, total] so a malformed cu_seqlens array
 // cannot move any access outside the tensors.

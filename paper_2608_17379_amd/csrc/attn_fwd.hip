@@ -50,7 +50,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   const int lane = tid & 63, wave = wave_id();
   const int l32 = lane & 31, half = lane >> 5;
 
-  const Layout& L = a.L;
+  const Layout L = a.L;
   const int z = blockIdx.x / L.Hq, h = blockIdx.x % L.Hq;
   const int hk = h / L.group;
   const Segment seg = segment_of(L, z);
@@ -58,12 +58,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   const int q0 = qt * kBM;
   if (q0 >= seg.len) return;
 
-  const int64_t qoff = (L.cu ? (int64_t)seg.start * L.q_row : (int64_t)z * L.q_batch) +
+  const int64_t qoff = (int64_t)seg.start * L.q_row + (int64_t)z * L.q_batch +
                        (int64_t)h * L.q_head;
-  const int64_t kvoff = (L.cu ? (int64_t)seg.start * L.kv_row : (int64_t)z * L.kv_batch) +
+  const int64_t kvoff = (int64_t)seg.start * L.kv_row + (int64_t)z * L.kv_batch +
                         (int64_t)hk * L.kv_head;
-  const int64_t roff = (L.cu ? (int64_t)seg.start : (int64_t)z * L.r_batch) +
-                       (int64_t)h * L.r_head;
+  const int64_t roff = (int64_t)seg.start + (int64_t)z * L.r_batch + (int64_t)h * L.r_head;
   const uint16_t* kp = a.k + kvoff;
   const uint16_t* vp = a.v + kvoff;
 
@@ -94,8 +93,13 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   float mref = -INFINITY;   // reference max of scale*log2(e)*s for query qrow
   float lsum = 0.f;         // this lane's share of the row sum, relative to mref
   const float sl2 = a.scale_log2;
+  // Fields used inside the lambdas below, as plain values (capturing the
+  // kernel argument itself can make the compiler spill it to scratch).
+  const bool causal = a.causal != 0;
+  const int len = seg.len;
+  const int64_t kv_row = L.kv_row;
 
-  auto compute = [&](int kt, const uint16_t* kt_lds, const uint16_t* vt_lds) {
+  auto compute = [&](int kt, const uint16_t* kt_lds, const uint16_t* vt_lds) __attribute__((always_inline)) {
     const int k0 = kt * kBN;
     f32x16 s[2];
 #pragma unroll
@@ -165,19 +169,19 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   // the barrier, which also frees the stage read one tile earlier), start the
   // next tile's loads into that stage, then compute.
   auto step = [&](int kt, bool work, const uint16_t* kc, const uint16_t* vc, uint16_t* kn,
-                  uint16_t* vn) {
+                  uint16_t* vn) __attribute__((always_inline)) {
     wait_vm<0>();
     __syncthreads();
     if (kt + 1 < nkt) {
-      dma.load(rows_rsrc(kp, (kt + 1) * kBN, seg.len, L.kv_row), kn, wave);
-      dma.load(rows_rsrc(vp, (kt + 1) * kBN, seg.len, L.kv_row), vn, wave);
+      dma.load(rows_rsrc(kp, (kt + 1) * kBN, len, kv_row), kn, wave);
+      dma.load(rows_rsrc(vp, (kt + 1) * kBN, len, kv_row), vn, wave);
     }
     if (work) compute(kt, kc, vc);
   };
 
   // Tiles past this wavefront's last query are fully masked for it: the
   // wavefront only joins their barriers and loads.
-  const int nkt_w = a.causal ? min(nkt, (qw0 + 31) / kBN + 1) : nkt;
+  const int nkt_w = causal ? min(nkt, (qw0 + 31) / kBN + 1) : nkt;
   if (nkt > 0) {
     dma.load(rows_rsrc(kp, 0, seg.len, L.kv_row), sk0, wave);
     dma.load(rows_rsrc(vp, 0, seg.len, L.kv_row), sv0, wave);
@@ -216,6 +220,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
     if (half == 0) a.lse[roff + qrow] = lsum > 0.f ? (mref + log2f(lsum)) * kLn2 : -INFINITY;
   }
 }
+
+// Explicit instantiations: without them the host compiler may skip the
+// launch stubs of these templates (leaving undefined symbols in the library).
+template __global__ void fwd_kernel<64>(FwdArgs);
+template __global__ void fwd_kernel<128>(FwdArgs);
 
 }  // namespace
 

@@ -2,8 +2,10 @@
 //
 // A "segment" is one batch entry (fixed length) or one packed sequence.  Row i
 // of head h of segment z of a q-like tensor (q, o, dO, dq; Hq heads) is at
-//   base + seg_off + h * head_stride + i * row_stride       (elements)
-// with seg_off = z * batch_stride (fixed) or cu[z] * row_stride (packed);
+//   base + start * row_stride + z * batch_stride + h * head_stride
+//        + i * row_stride                                    (elements)
+// where start = cu[z] and batch_stride = 0 for packed input, and start = 0
+// for fixed-length input;
 // k-like tensors (k, v, dk, dv; Hkv heads) use the kv strides.  Row-indexed
 // fp32 arrays (lse, Delta) follow the same rule with their own strides and a
 // unit row stride.

@@ -227,24 +227,47 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(BwdArgs a) {
 
 // ---------------------------------------------------------------------------
 // dK, dV
+//
+// Eight wavefronts per workgroup of 128 keys: wavefronts w and w + 4 (which
+// share a SIMD) own the same 32 keys and take the two 32-query halves of
+// every 64-query tile, so each SIMD runs two independent wavefronts whose
+// MFMA, VALU and LDS work interleave in hardware.  K and V of the
+// workgroup's keys stay in LDS (read as B operands), the query-side tiles
+// (Q, dO, L, Delta) stream through two LDS stages, and the two partial dK/dV
+// accumulators of each key are added through LDS at the end.
 // ---------------------------------------------------------------------------
-constexpr int kKN = 128;   // keys per workgroup
+constexpr int kKN = 128;        // keys per workgroup
+constexpr int kDkvWaves = 8;
+constexpr int kDkvThreads = 64 * kDkvWaves;
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
-  using Tile = AsyncTile<D>;
-  __shared__ __attribute__((aligned(1024))) uint16_t sq0[Tile::ELEMS];
-  __shared__ __attribute__((aligned(1024))) uint16_t sq1[Tile::ELEMS];
-  __shared__ __attribute__((aligned(1024))) uint16_t sdo0[Tile::ELEMS];
-  __shared__ __attribute__((aligned(1024))) uint16_t sdo1[Tile::ELEMS];
-  __shared__ __attribute__((aligned(16))) float sl0[kTileRows];
-  __shared__ __attribute__((aligned(16))) float sl1[kTileRows];
-  __shared__ __attribute__((aligned(16))) float sd0[kTileRows];
-  __shared__ __attribute__((aligned(16))) float sd1[kTileRows];
+struct DkvSmem {
+  static constexpr int TILE = 64 * D * 2;                  // bytes of a 64-row bf16 tile
+  static constexpr int K = 0;                              // 2 tiles: keys 0-63, 64-127
+  static constexpr int V = K + 2 * TILE;
+  static constexpr int Q = V + 2 * TILE;                   // 2 stages
+  static constexpr int DO = Q + 2 * TILE;                  // 2 stages
+  static constexpr int LSE = DO + 2 * TILE;                // 2 stages x 64 fp32
+  static constexpr int DEL = LSE + 2 * 256;
+  static constexpr int BYTES = DEL + 2 * 256;
+  // partial dK/dV of wavefronts 4..7: (D/32) x 2 f32x16 per lane
+  static constexpr int RED_SLOTS = (D / 32) * 2 * 4;       // u32x4 slots per lane
+  static_assert(4 * RED_SLOTS * 1024 <= BYTES, "reduction buffer");
+};
+
+template <int D, bool CAUSAL>
+__global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
+  using Tile = AsyncTile<D, kDkvWaves>;
+  using SM = DkvSmem<D>;
+  __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
+  uint16_t* const sk = reinterpret_cast<uint16_t*>(smem + SM::K);
+  uint16_t* const sv = reinterpret_cast<uint16_t*>(smem + SM::V);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = wave_id();
   const int l32 = lane & 31, half = lane >> 5;
+  const int kq = wave & 3;    // 32-key group
+  const int sb = wave >> 2;   // which 32-query half of each tile
 
   const Layout L = a.L;
   const int z = blockIdx.x / L.Hkv, hk = blockIdx.x % L.Hkv;
@@ -257,32 +280,60 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
   const int64_t qseg = (int64_t)seg.start * L.q_row + (int64_t)z * L.q_batch;
   const int64_t rseg = (int64_t)seg.start + (int64_t)z * L.r_batch;
 
-  const int kw0 = k0 + wave * 32;
+  const int kw0 = k0 + kq * 32;
   const int krow = kw0 + l32;
-  const bool kvalid = krow < seg.len;
   // Fields used inside the lambdas below, as plain values (capturing the
   // kernel argument itself would make the compiler spill it to scratch).
   const uint16_t* const qbase = a.q;
   const uint16_t* const dobase = a.dout;
   const float* const lsebase = a.lse;
   const float* const delbase = a.delta;
-  const bool causal = a.causal != 0;
   const int group = L.group;
-  const int64_t q_head = L.q_head, q_row = L.q_row, r_head = L.r_head;
+  const int64_t q_head = L.q_head, r_head = L.r_head;
+  const int64_t q_row_b = L.q_row * 2;
   const int len = seg.len;
+  const float sl2 = a.scale_log2;
 
-  // K and V rows of this lane's key as B operands of S = Q K^T, dP = dO V^T.
-  u32x4 kreg[D / 16], vreg[D / 16];
+  // Iterations run over (group head g, query tile it) with it from the first
+  // tile that can see key k0.
+  const int it0 = CAUSAL ? k0 / kTileRows : 0;
+  const int nqt = (seg.len + kTileRows - 1) / kTileRows;
+  const int per_head = nqt - it0;
+  const int niter = per_head * L.group;
+
+  const Tile qdma(wave, lane, (int)q_row_b);
+  const RowReader<D> rr(l32, half);
+  const TransReader<D> trr(lane);
+  const uint32_t sbase = lds_addr(smem);
+
+  // K and V rows of the workgroup (once).
   {
-    const rsrc_t rk = rows_rsrc(a.k + kvoff, kw0, seg.len, L.kv_row);
-    const rsrc_t rv = rows_rsrc(a.v + kvoff, kw0, seg.len, L.kv_row);
-    const int base = l32 * (int)(L.kv_row * 2) + 16 * half;
+    const Tile kvdma(wave, lane, (int)(L.kv_row * 2));
+    const int64_t kv_row_b = L.kv_row * 2;
 #pragma unroll
-    for (int c = 0; c < D / 16; ++c) {
-      kreg[c] = bload16(rk, base + 32 * c);
-      vreg[c] = bload16(rv, base + 32 * c);
+    for (int t = 0; t < 2; ++t) {
+      dma_tile<D>(kvdma, rows_desc(a.k + kvoff, k0 + 64 * t, len, kv_row_b),
+                  sbase + SM::K + t * SM::TILE, wave);
+      dma_tile<D>(kvdma, rows_desc(a.v + kvoff, k0 + 64 * t, len, kv_row_b),
+                  sbase + SM::V + t * SM::TILE, wave);
     }
   }
+
+  auto issue = [&](int n, int st) __attribute__((always_inline)) {
+    const int g = n / per_head;
+    const int qb = (it0 + n % per_head) * kTileRows;
+    const int h = hk * group + g;
+    const int64_t qoff = qseg + (int64_t)h * q_head;
+    dma_tile<D>(qdma, rows_desc(qbase + qoff, qb, len, q_row_b), sbase + SM::Q + st * SM::TILE,
+                wave);
+    dma_tile<D>(qdma, rows_desc(dobase + qoff, qb, len, q_row_b), sbase + SM::DO + st * SM::TILE,
+                wave);
+    if (wave == 0 && lane < 16) {
+      const int64_t r = rseg + (int64_t)h * r_head;
+      dma16(rows_desc(lsebase + r, qb, len, 4), sbase + SM::LSE + st * 256, 16 * lane);
+      dma16(rows_desc(delbase + r, qb, len, 4), sbase + SM::DEL + st * 256, 16 * lane);
+    }
+  };
 
   f32x16 dkacc[D / 32], dvacc[D / 32];
 #pragma unroll
@@ -293,133 +344,115 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
       dvacc[db][r] = 0.f;
     }
 
-  // Iterations run over (group head g, query tile it) with it from the first
-  // tile that can see key k0.
-  const int it0 = a.causal ? k0 / kTileRows : 0;
-  const int nqt = (seg.len + kTileRows - 1) / kTileRows;
-  const int per_head = nqt - it0;
-  const int niter = per_head * L.group;
+  // This wavefront's K and V rows: tile kq / 2, rows 32 (kq % 2) + l32.
+  const uint16_t* const krd = sk + (kq >> 1) * (SM::TILE / 2) + 32 * (kq & 1) * D;
+  const uint16_t* const vrd = sv + (kq >> 1) * (SM::TILE / 2) + 32 * (kq & 1) * D;
 
-  const Tile dma(wave, lane, (int)(L.q_row * 2));
-  const RowReader<D> rr(l32, half);
-  const TransReader<D> trr(lane);
-  const float sl2 = a.scale_log2;
-
-  auto issue = [&](int n, uint16_t* q, uint16_t* dout, float* lse, float* del) __attribute__((always_inline)) {
-    const int g = n / per_head;
-    const int qb = (it0 + n % per_head) * kTileRows;
-    const int h = hk * group + g;
-    const int64_t qoff = qseg + (int64_t)h * q_head;
-    dma.load(rows_rsrc(qbase + qoff, qb, len, q_row), q, wave);
-    dma.load(rows_rsrc(dobase + qoff, qb, len, q_row), dout, wave);
-    const int64_t r = rseg + (int64_t)h * r_head;
-    if (wave == 0) {
-      load_rowvec(lsebase + r, qb, len, lse, lane);
-      load_rowvec(delbase + r, qb, len, del, lane);
+  auto compute = [&](int n, int st) __attribute__((always_inline)) {
+    const uint16_t* q = reinterpret_cast<const uint16_t*>(smem + SM::Q + st * SM::TILE);
+    const uint16_t* dout = reinterpret_cast<const uint16_t*>(smem + SM::DO + st * SM::TILE);
+    const float* lse = reinterpret_cast<const float*>(smem + SM::LSE + st * 256);
+    const float* del = reinterpret_cast<const float*>(smem + SM::DEL + st * 256);
+    const int qs0 = (it0 + n % per_head) * kTileRows + 32 * sb;
+    // S = Q K^T, dP = dO V^T for this wavefront's 32 queries x 32 keys.
+    f32x16 s, dp;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      s[r] = 0.f;
+      dp[r] = 0.f;
     }
-  };
-
-  auto compute = [&](int n, const uint16_t* q, const uint16_t* dout, const float* lse,
-                     const float* del) __attribute__((always_inline)) {
-    const int qb = (it0 + n % per_head) * kTileRows;
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      f32x16 s, dp;
+    for (int c = 0; c < D / 16; ++c) {
+      const int o = rr.rm[c] + 32 * sb * D;
+      s = mfma32(ld16(q + o), ld16(krd + rr.rm[c]), s);
+      dp = mfma32(ld16(dout + o), ld16(vrd + rr.rm[c]), dp);
+    }
+    // s[r], dp[r]: query qs0 + 8(r/4) + 4half + r%4, key krow.
+    const int t = krow - qs0 - 4 * half;   // key minus the lane's first query
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[r] = 0.f;
-        dp[r] = 0.f;
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse[32 * sb + 8 * g + 4 * half]);
+      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&del[32 * sb + 8 * g + 4 * half]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 4 * g + i;
+        float p = fast_exp2(__builtin_fmaf(s[r], sl2, -l4[i] * kLog2e));
+        if constexpr (CAUSAL) p = t > 8 * g + i ? 0.f : p;   // key after query
+        s[r] = p;
+        dp[r] = p * (dp[r] - d4[i]);
       }
+    }
+    // dV^T[d][key] += sum_q dO^T[d][q] P[q][key];  dK^T += Q^T dS, with the
+    // A operands read transposed out of the row-major dO and Q tiles.
 #pragma unroll
-      for (int c = 0; c < D / 16; ++c) {
-        const int o = rr.rm[c] + 32 * sb * D;
-        s = mfma32(ld16(q + o), kreg[c], s);
-        dp = mfma32(ld16(dout + o), vreg[c], dp);
-      }
-      // s[r], dp[r]: query qb + 32sb + 8(r/4) + 4half + r%4, key krow.
+    for (int c = 0; c < 2; ++c) {
+      const u32x4 pb = pack_chunk(s, c);
+      const u32x4 dsb = pack_chunk(dp, c);
+      const int rc = 16 * (2 * sb + c) * D;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse[32 * sb + 8 * g + 4 * half]);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          s[4 * g + i] = fast_exp2(__builtin_fmaf(s[4 * g + i], sl2, -l4[i] * kLog2e));
-      }
-      if (causal && qb + 32 * sb < kw0 + 31) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int q = qb + 32 * sb + 8 * (r / 4) + 4 * half + (r % 4);
-          s[r] = krow > q ? 0.f : s[r];
-        }
-      }
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(&del[32 * sb + 8 * g + 4 * half]);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) dp[4 * g + i] = s[4 * g + i] * (dp[4 * g + i] - d4[i]);   // dS
-      }
-      // dV^T[d][key] += sum_q dO^T[d][q] P[q][key];  dK^T += Q^T dS; the A
-      // operands are read transposed out of the row-major dO and Q tiles.
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const u32x4 pb = pack_chunk(s, c);
-        const u32x4 dsb = pack_chunk(dp, c);
-        const int rc = 16 * (2 * sb + c) * D;
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          const u32x2 dlo = ld_tr(dout + trr.tr[db][0] + rc), dhi = ld_tr(dout + trr.tr[db][1] + rc);
-          dvacc[db] = mfma32(u32x4{dlo[0], dlo[1], dhi[0], dhi[1]}, pb, dvacc[db]);
-          const u32x2 qlo = ld_tr(q + trr.tr[db][0] + rc), qhi = ld_tr(q + trr.tr[db][1] + rc);
-          dkacc[db] = mfma32(u32x4{qlo[0], qlo[1], qhi[0], qhi[1]}, dsb, dkacc[db]);
-        }
+      for (int db = 0; db < D / 32; ++db) {
+        const u32x2 dlo = ld_tr(dout + trr.tr[db][0] + rc), dhi = ld_tr(dout + trr.tr[db][1] + rc);
+        dvacc[db] = mfma32(u32x4{dlo[0], dlo[1], dhi[0], dhi[1]}, pb, dvacc[db]);
+        const u32x2 qlo = ld_tr(q + trr.tr[db][0] + rc), qhi = ld_tr(q + trr.tr[db][1] + rc);
+        dkacc[db] = mfma32(u32x4{qlo[0], qlo[1], qhi[0], qhi[1]}, dsb, dkacc[db]);
       }
     }
   };
 
-  auto step0 = [&](int n) __attribute__((always_inline)) {   // compute from stage 0, prefetch into stage 1
-    wait_vm<0>();
+  issue(0, 0);
+  for (int n = 0; n < niter; ++n) {
+    // Tile n has landed for this wavefront once its DMAs are done; the
+    // barrier makes every wavefront's share visible and frees the stage
+    // read at n - 1, which the loads of tile n + 1 now fill.
+    wait_vm_all();
     __syncthreads();
-    if (n + 1 < niter) issue(n + 1, sq1, sdo1, sl1, sd1);
-    compute(n, sq0, sdo0, sl0, sd0);
-  };
-  auto step1 = [&](int n) __attribute__((always_inline)) {   // compute from stage 1, prefetch into stage 0
-    wait_vm<0>();
-    __syncthreads();
-    if (n + 1 < niter) issue(n + 1, sq0, sdo0, sl0, sd0);
-    compute(n, sq1, sdo1, sl1, sd1);
-  };
-
-  if (niter > 0) issue(0, sq0, sdo0, sl0, sd0);
-  wait_vm<0>();
-  int n = 0;
-  for (; n + 1 < niter; n += 2) {
-    step0(n);
-    step1(n + 1);
+    if (n + 1 < niter) issue(n + 1, (n + 1) & 1);
+    compute(n, n & 1);
   }
-  if (n < niter) step0(n);
 
-  if (kvalid) {
-    const int64_t off = kvoff + (int64_t)krow * L.kv_row;
+  // Add the two partial accumulators of each key through LDS.
+  __syncthreads();
+  u32x4* const red = reinterpret_cast<u32x4*>(smem);
+  if (sb == 1) {
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        u32x2 wk, wv;
-        wk[0] = pack_bf16(dkacc[db][4 * g + 0] * a.scale, dkacc[db][4 * g + 1] * a.scale);
-        wk[1] = pack_bf16(dkacc[db][4 * g + 2] * a.scale, dkacc[db][4 * g + 3] * a.scale);
-        wv[0] = pack_bf16(dvacc[db][4 * g + 0], dvacc[db][4 * g + 1]);
-        wv[1] = pack_bf16(dvacc[db][4 * g + 2], dvacc[db][4 * g + 3]);
-        st8(a.dk + off + 32 * db + 8 * g + 4 * half, wk);
-        st8(a.dv + off + 32 * db + 8 * g + 4 * half, wv);
+      for (int j = 0; j < 4; ++j) {
+        const int slot = (kq * SM::RED_SLOTS + (2 * db) * 4 + j) * 64 + lane;
+        red[slot] = u32x4{__float_as_uint(dkacc[db][4 * j]), __float_as_uint(dkacc[db][4 * j + 1]),
+                          __float_as_uint(dkacc[db][4 * j + 2]), __float_as_uint(dkacc[db][4 * j + 3])};
+        red[slot + 4 * 64] = u32x4{__float_as_uint(dvacc[db][4 * j]), __float_as_uint(dvacc[db][4 * j + 1]),
+                                   __float_as_uint(dvacc[db][4 * j + 2]), __float_as_uint(dvacc[db][4 * j + 3])};
       }
   }
+  __syncthreads();
+  if (sb == 1 || krow >= len) return;
+  const int64_t off = kvoff + (int64_t)krow * L.kv_row;
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int slot = (kq * SM::RED_SLOTS + (2 * db) * 4 + j) * 64 + lane;
+      const u32x4 pk = red[slot], pv = red[slot + 4 * 64];
+      float dk[4], dv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        dk[i] = (dkacc[db][4 * j + i] + __uint_as_float(pk[i])) * a.scale;
+        dv[i] = dvacc[db][4 * j + i] + __uint_as_float(pv[i]);
+      }
+      st8(a.dk + off + 32 * db + 8 * j + 4 * half, u32x2{pack_bf16(dk[0], dk[1]), pack_bf16(dk[2], dk[3])});
+      st8(a.dv + off + 32 * db + 8 * j + 4 * half, u32x2{pack_bf16(dv[0], dv[1]), pack_bf16(dv[2], dv[3])});
+    }
 }
 
 // Explicit instantiations: without them the host compiler may skip the
 // launch stubs of these templates (leaving undefined symbols in the library).
 template __global__ void bwd_dq_kernel<64>(BwdArgs);
 template __global__ void bwd_dq_kernel<128>(BwdArgs);
-template __global__ void bwd_dkdv_kernel<64>(BwdArgs);
-template __global__ void bwd_dkdv_kernel<128>(BwdArgs);
+template __global__ void bwd_dkdv_kernel<64, false>(BwdArgs);
+template __global__ void bwd_dkdv_kernel<64, true>(BwdArgs);
+template __global__ void bwd_dkdv_kernel<128, false>(BwdArgs);
+template __global__ void bwd_dkdv_kernel<128, true>(BwdArgs);
 
 }  // namespace
 
@@ -433,10 +466,17 @@ hipError_t launch_bwd(const BwdArgs& a, int D, int phases, hipStream_t stream) {
       hipLaunchKernelGGL(bwd_dq_kernel<128>, gq, dim3(kThreads), 0, stream, a);
   }
   if (phases & 2) {
-    if (D == 64)
-      hipLaunchKernelGGL(bwd_dkdv_kernel<64>, gk, dim3(kThreads), 0, stream, a);
-    else
-      hipLaunchKernelGGL(bwd_dkdv_kernel<128>, gk, dim3(kThreads), 0, stream, a);
+    if (D == 64) {
+      if (a.causal)
+        hipLaunchKernelGGL((bwd_dkdv_kernel<64, true>), gk, dim3(kDkvThreads), 0, stream, a);
+      else
+        hipLaunchKernelGGL((bwd_dkdv_kernel<64, false>), gk, dim3(kDkvThreads), 0, stream, a);
+    } else {
+      if (a.causal)
+        hipLaunchKernelGGL((bwd_dkdv_kernel<128, true>), gk, dim3(kDkvThreads), 0, stream, a);
+      else
+        hipLaunchKernelGGL((bwd_dkdv_kernel<128, false>), gk, dim3(kDkvThreads), 0, stream, a);
+    }
   }
   return hipGetLastError();
 }

@@ -179,11 +179,12 @@ __device__ __forceinline__ int tile_swz(int r) {
     return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
 }
 
-template <int D>
+template <int D, int NW = 4>
 struct AsyncTile {
   static constexpr int CPR = D / 8;          // 16-byte chunks per row
-  static constexpr int NJ = CPR / 4;         // DMA instructions per wavefront (4 wavefronts)
+  static constexpr int NJ = CPR / NW;        // DMA instructions per wavefront (64 rows)
   static constexpr int ELEMS = 64 * D;       // bf16 elements per tile
+  static_assert(NJ * NW * 64 == 64 * CPR, "tile split");
   int goff[NJ];                              // this lane's source byte offset per instruction
   __device__ __forceinline__ AsyncTile(int wave, int lane, int row_bytes) {
 #pragma unroll
@@ -251,6 +252,71 @@ __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
+
+// ---------------------------------------------------------------------------
+// DMA through inline assembly, for tiles in a ring of LDS stages selected at
+// run time: the compiler does not model these loads as LDS writes, so it
+// adds no conservative waits before LDS reads of other stages.  Callers
+// order them explicitly (wait_vm + barrier before a stage is read, a barrier
+// after its last read before it is refilled).
+// ---------------------------------------------------------------------------
+typedef __attribute__((ext_vector_type(4))) int i32x4;
+
+// Raw buffer descriptor over [base, base + bytes) (gfx9 layout: 48-bit base,
+// stride 0, num_records, raw 32-bit data format).
+__device__ __forceinline__ i32x4 make_desc(const void* base, int64_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const int64_t lim = bytes < 0 ? 0 : (bytes > 0x7fffffff ? 0x7fffffff : bytes);
+  i32x4 d;
+  d[0] = (int)(uint32_t)a;
+  d[1] = (int)((uint32_t)(a >> 32) & 0xffffu);
+  d[2] = (int)lim;
+  d[3] = kRsrcFlags;
+  return d;
+}
+
+__device__ __forceinline__ i32x4 rows_desc(const void* head_base, int row0, int len,
+                                           int64_t row_stride_bytes) {
+  return make_desc(static_cast<const char*>(head_base) + (int64_t)row0 * row_stride_bytes,
+                   (int64_t)(len - row0) * row_stride_bytes);
+}
+
+// LDS byte address of a __shared__ object.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(ATTN_LDS const void*)p;
+}
+
+// One 16-byte-per-lane DMA: lane L's 16 bytes at byte voff of the buffer go
+// to LDS byte lds_base + 16 L.  M0 is saved and restored around the load.
+__device__ __forceinline__ void dma16(i32x4 desc, uint32_t lds_base, int voff) {
+  uint32_t saved;
+  lds_base = __builtin_amdgcn_readfirstlane(lds_base);
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_base), "v"(voff), "s"(desc)
+      : "memory");
+}
+
+template <int D, int NW>
+__device__ __forceinline__ void dma_tile(const AsyncTile<D, NW>& t, i32x4 desc, uint32_t tile_base,
+                                         int wave) {
+#pragma unroll
+  for (int j = 0; j < AsyncTile<D, NW>::NJ; ++j)
+    dma16(desc, tile_base + (uint32_t)((wave * AsyncTile<D, NW>::NJ + j) * 64 * 16), t.goff[j]);
+}
+
+// Wait for this wavefront's vector-memory operations, including the DMAs
+// above, which the compiler does not count.
+__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Scheduling-group masks for __builtin_amdgcn_sched_group_barrier.
+constexpr int kSgMfma = 0x008;
+constexpr int kSgValu = 0x002;
+constexpr int kSgDsRead = 0x100;
 
 // Resolve segment z of a layout: first row offset (elements) and length.
 // Packed offsets are clamped into [0, total] so a malformed cu_seqlens array

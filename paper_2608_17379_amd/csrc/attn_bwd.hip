@@ -31,41 +31,52 @@
 // The backward expects a finite L for every row that has a visible key (as
 // the forward produces); rows past the segment end read L = Delta = 0 and
 // contribute nothing, because their dO rows read as zero.
+#include <type_traits>
+
 #include "attn_kernels.hpp"
 #include "device_common.hpp"
 
 namespace attn {
 namespace {
 
-constexpr int kThreads = 256;
 constexpr int kTileRows = 64;
-
-// Enqueue rows [row0, row0 + 64) of an fp32 row vector (L or Delta of one
-// head) into a 256-byte LDS array: 16 lanes of one wavefront, 16 bytes each.
-__device__ __forceinline__ void load_rowvec(const float* head_base, int row0, int len, float* dst,
-                                            int lane) {
-  if (lane < 16) {
-    const rsrc_t r = make_rsrc(head_base + row0, (int64_t)(len - row0) * 4);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (ATTN_LDS void*)dst, 16, 16 * lane, 0, 0, 0);
-  }
-}
 
 // ---------------------------------------------------------------------------
 // dQ (and Delta)
+//
+// Eight wavefronts per workgroup of 128 query rows: wavefronts w and w + 4
+// (which share a SIMD) own the same 32 rows and take the two 32-key halves of
+// every 64-key tile, so each SIMD runs two independent wavefronts.  K and V
+// tiles stream through two LDS stages; the two partial dQ accumulators of
+// each row are added through LDS at the end.
 // ---------------------------------------------------------------------------
 constexpr int kQM = 128;   // query rows per workgroup
+constexpr int kDqWaves = 8;
+constexpr int kDqThreads = 64 * kDqWaves;
+
+constexpr int kDqStages = 3;   // K/V ring depth: tiles are loaded two ahead
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(BwdArgs a) {
-  using Tile = AsyncTile<D>;
-  __shared__ __attribute__((aligned(1024))) uint16_t sk0[Tile::ELEMS];
-  __shared__ __attribute__((aligned(1024))) uint16_t sk1[Tile::ELEMS];
-  __shared__ __attribute__((aligned(1024))) uint16_t sv0[Tile::ELEMS];
-  __shared__ __attribute__((aligned(1024))) uint16_t sv1[Tile::ELEMS];
+struct DqSmem {
+  static constexpr int TILE = 64 * D * 2;                  // bytes of a 64-row bf16 tile
+  static constexpr int K = 0;                              // kDqStages stages
+  static constexpr int V = K + kDqStages * TILE;           // kDqStages stages
+  static constexpr int BYTES = V + kDqStages * TILE;
+  static constexpr int RED_SLOTS = (D / 32) * 4;           // u32x4 slots per lane (dQ partial)
+  static_assert(4 * RED_SLOTS * 1024 <= BYTES, "reduction buffer");
+};
+
+template <int D, bool CAUSAL>
+__global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdArgs a) {
+  using Tile = AsyncTile<D, kDqWaves>;
+  using SM = DqSmem<D>;
+  __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = wave_id();
   const int l32 = lane & 31, half = lane >> 5;
+  const int qg = wave & 3;    // 32-row group
+  const int kb = wave >> 2;   // which 32-key half of each tile
 
   const Layout L = a.L;
   const int z = blockIdx.x / L.Hq, h = blockIdx.x % L.Hq;
@@ -80,20 +91,24 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(BwdArgs a) {
   const int64_t kvoff = (int64_t)seg.start * L.kv_row + (int64_t)z * L.kv_batch +
                         (int64_t)hk * L.kv_head;
   const int64_t roff = (int64_t)seg.start + (int64_t)z * L.r_batch + (int64_t)h * L.r_head;
-  const uint16_t* kp = a.k + kvoff;
-  const uint16_t* vp = a.v + kvoff;
+  const uint16_t* const kp = a.k + kvoff;
+  const uint16_t* const vp = a.v + kvoff;
+  const int64_t kv_row_b = L.kv_row * 2;
+  const int len = seg.len;
+  const float sl2 = a.scale_log2;
 
-  const int qw0 = q0 + wave * 32;
+  const int qw0 = q0 + qg * 32;
   const int qrow = qw0 + l32;
-  const bool valid = qrow < seg.len;
+  const bool valid = qrow < len;
 
-  // Q^T and dO^T as B operands; Delta from dO and O in the same layout.
+  // Q^T and dO^T as B operands; Delta from dO and O in the same layout
+  // (computed by the kb = 0 wavefront of each pair, which stores it).
   u32x4 qreg[D / 16], doreg[D / 16];
   float dsum = 0.f;
   {
-    const rsrc_t rq = rows_rsrc(a.q + qoff, qw0, seg.len, L.q_row);
-    const rsrc_t rdo = rows_rsrc(a.dout + qoff, qw0, seg.len, L.q_row);
-    const rsrc_t ro = rows_rsrc(a.o + qoff, qw0, seg.len, L.q_row);
+    const rsrc_t rq = rows_rsrc(a.q + qoff, qw0, len, L.q_row);
+    const rsrc_t rdo = rows_rsrc(a.dout + qoff, qw0, len, L.q_row);
+    const rsrc_t ro = rows_rsrc(a.o + qoff, qw0, len, L.q_row);
     const int base = l32 * (int)(L.q_row * 2) + 16 * half;
 #pragma unroll
     for (int c = 0; c < D / 16; ++c) {
@@ -109,22 +124,19 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(BwdArgs a) {
   float lse2 = 0.f;
   if (valid) {
     lse2 = a.lse[roff + qrow] * kLog2e;
-    if (half == 0) a.delta[roff + qrow] = delta;
+    if (kb == 0 && half == 0) a.delta[roff + qrow] = delta;
   }
 
-  const int kend = a.causal ? min(seg.len, q0 + kQM) : seg.len;
+  const int kend = CAUSAL ? min(len, q0 + kQM) : len;
   const int nkt = (kend + kTileRows - 1) / kTileRows;
-  // Key tiles past this wavefront's last query are fully masked for it.
-  const int nkt_w = a.causal ? min(nkt, (qw0 + 31) / kTileRows + 1) : nkt;
+  // Key tiles whose keys in this wavefront's half all follow its last row
+  // are fully masked for it.
+  const int nkt_w = CAUSAL ? min(nkt, (qw0 + 31 - 32 * kb) / kTileRows + 1) : nkt;
 
-  const Tile dma(wave, lane, (int)(L.kv_row * 2));
+  const Tile dma(wave, lane, (int)kv_row_b);
   const RowReader<D> rr(l32, half);
   const TransReader<D> trr(lane);
-  const float sl2 = a.scale_log2;
-  // Fields used inside the lambdas below, as plain values.
-  const bool causal = a.causal != 0;
-  const int len = seg.len;
-  const int64_t kv_row = L.kv_row;
+  const uint32_t sbase = lds_addr(smem);
 
   f32x16 dqacc[D / 32];
 #pragma unroll
@@ -132,97 +144,122 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) dqacc[db][r] = 0.f;
 
-  auto compute = [&](int kt, const uint16_t* kc, const uint16_t* vc) __attribute__((always_inline)) {
-    const int k0 = kt * kTileRows;
-    f32x16 s[2], dp[2];
+  auto issue = [&](int kt, int st) __attribute__((always_inline)) {
+    dma_tile<D>(dma, rows_desc(kp, kt * kTileRows, len, kv_row_b), sbase + SM::K + st * SM::TILE,
+                wave);
+    dma_tile<D>(dma, rows_desc(vp, kt * kTileRows, len, kv_row_b), sbase + SM::V + st * SM::TILE,
+                wave);
+  };
+
+  // One tile of this wavefront's work (32 keys x 32 rows): S^T = K Q^T and
+  // dP^T = V dO^T, dS^T = P^T (dP^T - Delta) with P^T = exp2(s scale log2 e
+  // - L log2 e), then dQ^T += K^T dS^T with K^T read transposed.  Only tiles
+  // on the causal diagonal or holding the sequence end are masked.
+  auto compute = [&](int kt, int st, auto masked) __attribute__((always_inline)) {
+    const uint16_t* kc = reinterpret_cast<const uint16_t*>(smem + SM::K + st * SM::TILE);
+    const uint16_t* vc = reinterpret_cast<const uint16_t*>(smem + SM::V + st * SM::TILE);
+    f32x16 s, dp;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[kb][r] = 0.f;
-        dp[kb][r] = 0.f;
-      }
-#pragma unroll
-    for (int c = 0; c < D / 16; ++c)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const int o = rr.rm[c] + 32 * kb * D;
-        s[kb] = mfma32(ld16(kc + o), qreg[c], s[kb]);
-        dp[kb] = mfma32(ld16(vc + o), doreg[c], dp[kb]);
-      }
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] = fast_exp2(__builtin_fmaf(s[kb][r], sl2, -lse2));
-    if ((causal && k0 + kTileRows - 1 > qw0) || k0 + kTileRows > len) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = k0 + 32 * kb + 8 * (r / 4) + 4 * half + (r % 4);
-          s[kb][r] = ((causal && key > qrow) || key >= len) ? 0.f : s[kb][r];
-        }
+    for (int r = 0; r < 16; ++r) {
+      s[r] = 0.f;
+      dp[r] = 0.f;
     }
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int c = 0; c < D / 16; ++c) {
+      const int o = rr.rm[c] + 32 * kb * D;
+      s = mfma32(ld16(kc + o), qreg[c], s);
+      dp = mfma32(ld16(vc + o), doreg[c], dp);
+    }
+    // s[r]: key ks0 + 8(r/4) + 4half + r%4, query qrow.
+    const int ks0 = kt * kTileRows + 32 * kb;
+    const int t = ks0 + 4 * half - qrow;   // the lane's first key minus its query
+    const int u = ks0 + 4 * half - len;    // the lane's first key minus the end
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] = s[kb][r] * (dp[kb][r] - delta);   // dS^T
-    // dQ^T[d][q] += sum_key K^T[d][key] dS^T[key][q]; K^T read transposed.
+    for (int r = 0; r < 16; ++r) {
+      float p = fast_exp2(__builtin_fmaf(s[r], sl2, -lse2));
+      if constexpr (decltype(masked)::value) {
+        const int off = 8 * (r / 4) + (r % 4);
+        if constexpr (CAUSAL) p = t + off > 0 ? 0.f : p;   // key after query
+        p = u + off >= 0 ? 0.f : p;                        // key past the end
+      }
+      s[r] = p * (dp[r] - delta);
+    }
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const u32x4 b = pack_chunk(s[c >> 1], c & 1);
+    for (int c = 0; c < 2; ++c) {
+      const u32x4 b = pack_chunk(s, c);
+      const int rc = 16 * (2 * kb + c) * D;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
-        const u32x2 lo = ld_tr(kc + trr.tr[db][0] + 16 * c * D);
-        const u32x2 hi = ld_tr(kc + trr.tr[db][1] + 16 * c * D);
+        const u32x2 lo = ld_tr(kc + trr.tr[db][0] + rc), hi = ld_tr(kc + trr.tr[db][1] + rc);
         dqacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, b, dqacc[db]);
       }
     }
   };
-  auto step = [&](int kt, bool work, const uint16_t* kc, const uint16_t* vc, uint16_t* kn,
-                  uint16_t* vn) __attribute__((always_inline)) {
-    wait_vm<0>();
-    __syncthreads();
-    if (kt + 1 < nkt) {
-      dma.load(rows_rsrc(kp, (kt + 1) * kTileRows, len, kv_row), kn, wave);
-      dma.load(rows_rsrc(vp, (kt + 1) * kTileRows, len, kv_row), vn, wave);
-    }
-    if (work) compute(kt, kc, vc);
-  };
 
-  if (nkt > 0) {
-    dma.load(rows_rsrc(kp, 0, seg.len, L.kv_row), sk0, wave);
-    dma.load(rows_rsrc(vp, 0, seg.len, L.kv_row), sv0, wave);
-  }
-  wait_vm<0>();
-  int kt = 0;
-  for (; kt + 1 < nkt_w; kt += 2) {
-    step(kt, true, sk0, sv0, sk1, sv1);
-    step(kt + 1, true, sk1, sv1, sk0, sv0);
-  }
-  if (kt < nkt_w) {
-    step(kt, true, sk0, sv0, sk1, sv1);
-    ++kt;
-  }
-  for (; kt < nkt; ++kt) {
-    if (kt & 1)
-      step(kt, false, sk1, sv1, sk0, sv0);
+  // Ring of kDqStages stages, tiles issued kDqStages - 1 ahead.  At tile kt
+  // this wavefront waits for its own loads of tile kt (those of tile kt + 1
+  // may stay in flight), then the barrier makes all shares visible and frees
+  // the stage read at kt - 1, which tile kt + 2 now fills.
+  static_assert(kDqStages == 3, "wait counts below assume three stages");
+  constexpr int kLoadsPerTile = 2 * Tile::NJ;
+  // Tiles [0, nkt_u) need no mask for any row of the workgroup.
+  const int nkt_u = CAUSAL ? min(nkt, q0 / kTileRows)
+                           : (len % kTileRows == 0 ? nkt : nkt - 1);
+  int kt = 0, st = 0;
+  auto sync = [&]() __attribute__((always_inline)) {
+    if (kt + 1 < nkt)
+      wait_vm_upto<kLoadsPerTile>();
     else
-      step(kt, false, sk0, sv0, sk1, sv1);
+      wait_vm_all();
+    __syncthreads();
+    if (kt + 2 < nkt) issue(kt + 2, st == 0 ? 2 : st - 1);
+  };
+  auto advance = [&]() __attribute__((always_inline)) {
+    st = st == kDqStages - 1 ? 0 : st + 1;
+    ++kt;
+  };
+  if (nkt > 0) issue(0, 0);
+  if (nkt > 1) issue(1, 1);
+  while (kt < nkt_u) {
+    sync();
+    compute(kt, st, std::false_type{});
+    advance();
+  }
+  while (kt < nkt_w) {
+    sync();
+    compute(kt, st, std::true_type{});
+    advance();
+  }
+  while (kt < nkt) {   // fully masked for this wavefront: loads only
+    sync();
+    advance();
   }
 
-  if (valid) {
-    uint16_t* dqp = a.dq + qoff + (int64_t)qrow * L.q_row;
+  // Add the two partial accumulators of each row through LDS.
+  __syncthreads();
+  u32x4* const red = reinterpret_cast<u32x4*>(smem);
+  if (kb == 1) {
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        u32x2 w;
-        w[0] = pack_bf16(dqacc[db][4 * g + 0] * a.scale, dqacc[db][4 * g + 1] * a.scale);
-        w[1] = pack_bf16(dqacc[db][4 * g + 2] * a.scale, dqacc[db][4 * g + 3] * a.scale);
-        st8(dqp + 32 * db + 8 * g + 4 * half, w);
-      }
+      for (int j = 0; j < 4; ++j)
+        red[(qg * SM::RED_SLOTS + 4 * db + j) * 64 + lane] =
+            u32x4{__float_as_uint(dqacc[db][4 * j]), __float_as_uint(dqacc[db][4 * j + 1]),
+                  __float_as_uint(dqacc[db][4 * j + 2]), __float_as_uint(dqacc[db][4 * j + 3])};
   }
+  __syncthreads();
+  if (kb == 1 || !valid) return;
+  uint16_t* dqp = a.dq + qoff + (int64_t)qrow * L.q_row;
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const u32x4 pq = red[(qg * SM::RED_SLOTS + 4 * db + j) * 64 + lane];
+      float v[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = (dqacc[db][4 * j + i] + __uint_as_float(pq[i])) * a.scale;
+      st8(dqp + 32 * db + 8 * j + 4 * half, u32x2{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])});
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -447,8 +484,10 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
 
 // Explicit instantiations: without them the host compiler may skip the
 // launch stubs of these templates (leaving undefined symbols in the library).
-template __global__ void bwd_dq_kernel<64>(BwdArgs);
-template __global__ void bwd_dq_kernel<128>(BwdArgs);
+template __global__ void bwd_dq_kernel<64, false>(BwdArgs);
+template __global__ void bwd_dq_kernel<64, true>(BwdArgs);
+template __global__ void bwd_dq_kernel<128, false>(BwdArgs);
+template __global__ void bwd_dq_kernel<128, true>(BwdArgs);
 template __global__ void bwd_dkdv_kernel<64, false>(BwdArgs);
 template __global__ void bwd_dkdv_kernel<64, true>(BwdArgs);
 template __global__ void bwd_dkdv_kernel<128, false>(BwdArgs);
@@ -460,10 +499,17 @@ hipError_t launch_bwd(const BwdArgs& a, int D, int phases, hipStream_t stream) {
   const dim3 gq((unsigned)(a.L.nseg * a.L.Hq), (unsigned)((a.L.S + kQM - 1) / kQM));
   const dim3 gk((unsigned)(a.L.nseg * a.L.Hkv), (unsigned)((a.L.S + kKN - 1) / kKN));
   if (phases & 1) {
-    if (D == 64)
-      hipLaunchKernelGGL(bwd_dq_kernel<64>, gq, dim3(kThreads), 0, stream, a);
-    else
-      hipLaunchKernelGGL(bwd_dq_kernel<128>, gq, dim3(kThreads), 0, stream, a);
+    if (D == 64) {
+      if (a.causal)
+        hipLaunchKernelGGL((bwd_dq_kernel<64, true>), gq, dim3(kDqThreads), 0, stream, a);
+      else
+        hipLaunchKernelGGL((bwd_dq_kernel<64, false>), gq, dim3(kDqThreads), 0, stream, a);
+    } else {
+      if (a.causal)
+        hipLaunchKernelGGL((bwd_dq_kernel<128, true>), gq, dim3(kDqThreads), 0, stream, a);
+      else
+        hipLaunchKernelGGL((bwd_dq_kernel<128, false>), gq, dim3(kDqThreads), 0, stream, a);
+    }
   }
   if (phases & 2) {
     if (D == 64) {

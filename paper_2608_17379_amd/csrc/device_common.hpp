@@ -313,6 +313,13 @@ __device__ __forceinline__ void dma_tile(const AsyncTile<D, NW>& t, i32x4 desc, 
 // above, which the compiler does not count.
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Wait until at most N of them are in flight (loads complete in order).
+template <int N>
+__device__ __forceinline__ void wait_vm_upto() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 // Scheduling-group masks for __builtin_amdgcn_sched_group_barrier.
 constexpr int kSgMfma = 0x008;
 constexpr int kSgValu = 0x002;

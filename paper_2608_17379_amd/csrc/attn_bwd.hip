@@ -385,7 +385,7 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
   const uint16_t* const krd = sk + (kq >> 1) * (SM::TILE / 2) + 32 * (kq & 1) * D;
   const uint16_t* const vrd = sv + (kq >> 1) * (SM::TILE / 2) + 32 * (kq & 1) * D;
 
-  auto compute = [&](int n, int st) __attribute__((always_inline)) {
+  auto compute = [&](int n, int st, auto masked) __attribute__((always_inline)) {
     const uint16_t* q = reinterpret_cast<const uint16_t*>(smem + SM::Q + st * SM::TILE);
     const uint16_t* dout = reinterpret_cast<const uint16_t*>(smem + SM::DO + st * SM::TILE);
     const float* lse = reinterpret_cast<const float*>(smem + SM::LSE + st * 256);
@@ -414,7 +414,7 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
       for (int i = 0; i < 4; ++i) {
         const int r = 4 * g + i;
         float p = fast_exp2(__builtin_fmaf(s[r], sl2, -l4[i] * kLog2e));
-        if constexpr (CAUSAL) p = t > 8 * g + i ? 0.f : p;   // key after query
+        if constexpr (decltype(masked)::value) p = t > 8 * g + i ? 0.f : p;   // key after query
         s[r] = p;
         dp[r] = p * (dp[r] - d4[i]);
       }
@@ -436,15 +436,25 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
     }
   };
 
-  issue(0, 0);
-  for (int n = 0; n < niter; ++n) {
-    // Tile n has landed for this wavefront once its DMAs are done; the
-    // barrier makes every wavefront's share visible and frees the stage
-    // read at n - 1, which the loads of tile n + 1 now fill.
+  // Tile n has landed for this wavefront once its DMAs are done; the barrier
+  // makes every wavefront's share visible and frees the stage read at n - 1,
+  // which the loads of tile n + 1 now fill.  Only the first two query tiles
+  // of each head (those reaching below the causal diagonal of this
+  // workgroup's keys) are masked; rows past the end need no mask, as their
+  // Q and dO read as zero.
+  auto step = [&](int n, auto masked) __attribute__((always_inline)) {
     wait_vm_all();
     __syncthreads();
     if (n + 1 < niter) issue(n + 1, (n + 1) & 1);
-    compute(n, n & 1);
+    compute(n, n & 1, masked);
+  };
+  const int nmask = CAUSAL ? min(2, per_head) : 0;
+  issue(0, 0);
+  int n = 0;
+  for (int g = 0; g < group; ++g) {
+    const int nend = n + per_head;
+    for (const int nm = n + nmask; n < nm; ++n) step(n, std::true_type{});
+    for (; n < nend; ++n) step(n, std::false_type{});
   }
 
   // Add the two partial accumulators of each key through LDS.

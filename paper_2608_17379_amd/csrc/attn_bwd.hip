@@ -47,23 +47,24 @@ constexpr int kTileRows = 64;
 // Eight wavefronts per workgroup of 128 query rows: wavefronts w and w + 4
 // (which share a SIMD) own the same 32 rows and take the two 32-key halves of
 // every 64-key tile, so each SIMD runs two independent wavefronts.  K and V
-// tiles stream through two LDS stages; the two partial dQ accumulators of
+// tiles stream through a four-stage LDS ring; the two partial dQ accumulators of
 // each row are added through LDS at the end.
 // ---------------------------------------------------------------------------
 constexpr int kQM = 128;   // query rows per workgroup
 constexpr int kDqWaves = 8;
 constexpr int kDqThreads = 64 * kDqWaves;
 
-constexpr int kDqStages = 3;   // K/V ring depth: tiles are loaded two ahead
+constexpr int kDqStages = 4;   // K/V ring depth (a power of two)
 
 template <int D>
 struct DqSmem {
   static constexpr int TILE = 64 * D * 2;                  // bytes of a 64-row bf16 tile
   static constexpr int K = 0;                              // kDqStages stages
   static constexpr int V = K + kDqStages * TILE;           // kDqStages stages
-  static constexpr int BYTES = V + kDqStages * TILE;
-  static constexpr int RED_SLOTS = (D / 32) * 4;           // u32x4 slots per lane (dQ partial)
-  static_assert(4 * RED_SLOTS * 1024 <= BYTES, "reduction buffer");
+  static constexpr int X = V + kDqStages * TILE;           // 2 tiles, used by the prologue
+  static constexpr int BYTES = X + 2 * TILE;
+  // epilogue: half of a dQ partial per wavefront, (D/64) x 4 u32x4 per lane
+  static_assert(8 * (D / 64) * 4 * 1024 <= BYTES, "reduction buffer");
 };
 
 template <int D, bool CAUSAL>
@@ -101,42 +102,75 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdArgs a) {
   const int qrow = qw0 + l32;
   const bool valid = qrow < len;
 
-  // Q^T and dO^T as B operands; Delta from dO and O in the same layout
-  // (computed by the kb = 0 wavefront of each pair, which stores it).
-  u32x4 qreg[D / 16], doreg[D / 16];
-  float dsum = 0.f;
-  {
-    const rsrc_t rq = rows_rsrc(a.q + qoff, qw0, len, L.q_row);
-    const rsrc_t rdo = rows_rsrc(a.dout + qoff, qw0, len, L.q_row);
-    const rsrc_t ro = rows_rsrc(a.o + qoff, qw0, len, L.q_row);
-    const int base = l32 * (int)(L.q_row * 2) + 16 * half;
-#pragma unroll
-    for (int c = 0; c < D / 16; ++c) {
-      qreg[c] = bload16(rq, base + 32 * c);
-      doreg[c] = bload16(rdo, base + 32 * c);
-      const u32x4 ov = bload16(ro, base + 32 * c);
-#pragma unroll
-      for (int w = 0; w < 4; ++w)
-        dsum += bf16_lo(doreg[c][w]) * bf16_lo(ov[w]) + bf16_hi(doreg[c][w]) * bf16_hi(ov[w]);
-    }
-  }
-  const float delta = dsum + swap_halves(dsum);
-  float lse2 = 0.f;
-  if (valid) {
-    lse2 = a.lse[roff + qrow] * kLog2e;
-    if (kb == 0 && half == 0) a.delta[roff + qrow] = delta;
-  }
-
   const int kend = CAUSAL ? min(len, q0 + kQM) : len;
   const int nkt = (kend + kTileRows - 1) / kTileRows;
   // Key tiles whose keys in this wavefront's half all follow its last row
   // are fully masked for it.
   const int nkt_w = CAUSAL ? min(nkt, (qw0 + 31 - 32 * kb) / kTileRows + 1) : nkt;
+  // Tiles [0, nkt_u) need no mask for any row of the workgroup.
+  const int nkt_u = CAUSAL ? min(nkt, q0 / kTileRows)
+                           : (len % kTileRows == 0 ? nkt : nkt - 1);
 
   const Tile dma(wave, lane, (int)kv_row_b);
-  const RowReader<D> rr(l32, half);
-  const TransReader<D> trr(lane);
   const uint32_t sbase = lds_addr(smem);
+  auto issue = [&](int kt) __attribute__((always_inline)) {
+    const int st = kt & (kDqStages - 1);
+    dma_tile<D>(dma, rows_desc(kp, kt * kTileRows, len, kv_row_b), sbase + SM::K + st * SM::TILE,
+                wave);
+    dma_tile<D>(dma, rows_desc(vp, kt * kTileRows, len, kv_row_b), sbase + SM::V + st * SM::TILE,
+                wave);
+  };
+  const RowReader<D> rr(l32, half);
+
+  // Prologue: the workgroup's Q, dO and O rows go through LDS (one coalesced
+  // copy of each row instead of strided per-lane loads, repeated by both
+  // wavefronts of a pair), beside the first two K/V tiles.  The 64-row
+  // halves sit in the extra region (Q) and in stages 2 and 3 (dO, O), which
+  // the ring fills only after the rows have been read.
+  {
+    const Tile qdma(wave, lane, (int)(L.q_row * 2));
+    const int64_t q_row_b = L.q_row * 2;
+    auto rows = [&](const uint16_t* base, uint32_t lo, uint32_t hi) __attribute__((always_inline)) {
+      dma_tile<D>(qdma, rows_desc(base + qoff, q0, len, q_row_b), sbase + lo, wave);
+      dma_tile<D>(qdma, rows_desc(base + qoff, q0 + kTileRows, len, q_row_b), sbase + hi, wave);
+    };
+    rows(a.q, SM::X, SM::X + SM::TILE);
+    rows(a.dout, SM::K + 2 * SM::TILE, SM::V + 2 * SM::TILE);
+    rows(a.o, SM::K + 3 * SM::TILE, SM::V + 3 * SM::TILE);
+  }
+  if (nkt > 0) issue(0);
+  if (nkt > 1) issue(1);
+  float lse2 = 0.f;
+  if (valid) lse2 = a.lse[roff + qrow] * kLog2e;
+  wait_vm_all();
+  __syncthreads();
+
+  // Q^T and dO^T as B operands (this wavefront's 32 rows, in 64-row half
+  // qg / 2); Delta from dO and O in the same layout (stored by the kb = 0
+  // wavefront of each pair).
+  u32x4 qreg[D / 16], doreg[D / 16];
+  float dsum = 0.f;
+  {
+    const int sub = 32 * (qg & 1) * D;
+    const uint16_t* qs = reinterpret_cast<const uint16_t*>(smem + SM::X + (qg >> 1) * SM::TILE);
+    const uint16_t* dos = reinterpret_cast<const uint16_t*>(smem + ((qg >> 1) ? SM::V : SM::K) + 2 * SM::TILE);
+    const uint16_t* os = reinterpret_cast<const uint16_t*>(smem + ((qg >> 1) ? SM::V : SM::K) + 3 * SM::TILE);
+#pragma unroll
+    for (int c = 0; c < D / 16; ++c) {
+      qreg[c] = ld16(qs + rr.rm[c] + sub);
+      doreg[c] = ld16(dos + rr.rm[c] + sub);
+      const u32x4 ov = ld16(os + rr.rm[c] + sub);
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        dsum += bf16_lo(doreg[c][w]) * bf16_lo(ov[w]) + bf16_hi(doreg[c][w]) * bf16_hi(ov[w]);
+    }
+  }
+  __syncthreads();   // stages 2 and 3 are free for the ring
+  if (nkt > 2) issue(2);
+  const float delta = dsum + swap_halves(dsum);
+  if (valid && kb == 0 && half == 0) a.delta[roff + qrow] = delta;
+
+  const TransReader<D> trr(lane);
 
   f32x16 dqacc[D / 32];
 #pragma unroll
@@ -144,32 +178,29 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) dqacc[db][r] = 0.f;
 
-  auto issue = [&](int kt, int st) __attribute__((always_inline)) {
-    dma_tile<D>(dma, rows_desc(kp, kt * kTileRows, len, kv_row_b), sbase + SM::K + st * SM::TILE,
-                wave);
-    dma_tile<D>(dma, rows_desc(vp, kt * kTileRows, len, kv_row_b), sbase + SM::V + st * SM::TILE,
-                wave);
+  // One tile of this wavefront's work (32 keys x 32 rows):
+  //   S^T = K Q^T and dP^T = V dO^T (MFMA);
+  //   P^T = exp2(s scale log2 e - L log2 e), masked only on tiles at the
+  //   causal diagonal or the sequence end, and dS^T = P^T (dP^T - Delta),
+  //   packed to bf16 (VALU);
+  //   dQ^T += K^T dS^T with K^T read transposed (MFMA).
+  // The loop is software-pipelined so that each wavefront's MFMAs run under
+  // its own VALU work: tile kt's exponentials are issued beside its dP^T
+  // product, and its dS^T beside the S^T product of tile kt + 1.
+  auto kptr = [&](int kt) __attribute__((always_inline)) {
+    return reinterpret_cast<const uint16_t*>(smem + SM::K + (kt & (kDqStages - 1)) * SM::TILE);
   };
-
-  // One tile of this wavefront's work (32 keys x 32 rows): S^T = K Q^T and
-  // dP^T = V dO^T, dS^T = P^T (dP^T - Delta) with P^T = exp2(s scale log2 e
-  // - L log2 e), then dQ^T += K^T dS^T with K^T read transposed.  Only tiles
-  // on the causal diagonal or holding the sequence end are masked.
-  auto compute = [&](int kt, int st, auto masked) __attribute__((always_inline)) {
-    const uint16_t* kc = reinterpret_cast<const uint16_t*>(smem + SM::K + st * SM::TILE);
-    const uint16_t* vc = reinterpret_cast<const uint16_t*>(smem + SM::V + st * SM::TILE);
-    f32x16 s, dp;
+  auto vptr = [&](int kt) __attribute__((always_inline)) {
+    return reinterpret_cast<const uint16_t*>(smem + SM::V + (kt & (kDqStages - 1)) * SM::TILE);
+  };
+  auto score = [&](const uint16_t* tile, const u32x4 (&b)[D / 16], f32x16& acc)
+      __attribute__((always_inline)) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      s[r] = 0.f;
-      dp[r] = 0.f;
-    }
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 #pragma unroll
-    for (int c = 0; c < D / 16; ++c) {
-      const int o = rr.rm[c] + 32 * kb * D;
-      s = mfma32(ld16(kc + o), qreg[c], s);
-      dp = mfma32(ld16(vc + o), doreg[c], dp);
-    }
+    for (int c = 0; c < D / 16; ++c) acc = mfma32(ld16(tile + rr.rm[c] + 32 * kb * D), b[c], acc);
+  };
+  auto softmax = [&](int kt, f32x16& s, auto masked) __attribute__((always_inline)) {
     // s[r]: key ks0 + 8(r/4) + 4half + r%4, query qrow.
     const int ks0 = kt * kTileRows + 32 * kb;
     const int t = ks0 + 4 * half - qrow;   // the lane's first key minus its query
@@ -182,84 +213,155 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdArgs a) {
         if constexpr (CAUSAL) p = t + off > 0 ? 0.f : p;   // key after query
         p = u + off >= 0 ? 0.f : p;                        // key past the end
       }
-      s[r] = p * (dp[r] - delta);
+      s[r] = p;
     }
+  };
+  auto dscore = [&](f32x16& p, const f32x16& dp, u32x4 (&b)[2]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) p[r] = p[r] * (dp[r] - delta);
+    b[0] = pack_chunk(p, 0);
+    b[1] = pack_chunk(p, 1);
+  };
+  auto accum = [&](int kt, const u32x4 (&b)[2]) __attribute__((always_inline)) {
+    const uint16_t* kc = kptr(kt);
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      const u32x4 b = pack_chunk(s, c);
       const int rc = 16 * (2 * kb + c) * D;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
         const u32x2 lo = ld_tr(kc + trr.tr[db][0] + rc), hi = ld_tr(kc + trr.tr[db][1] + rc);
-        dqacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, b, dqacc[db]);
+        dqacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, b[c], dqacc[db]);
       }
     }
   };
 
-  // Ring of kDqStages stages, tiles issued kDqStages - 1 ahead.  At tile kt
-  // this wavefront waits for its own loads of tile kt (those of tile kt + 1
-  // may stay in flight), then the barrier makes all shares visible and frees
-  // the stage read at kt - 1, which tile kt + 2 now fills.
-  static_assert(kDqStages == 3, "wait counts below assume three stages");
+  // Ring of kDqStages stages.  At the top of tile kt this wavefront waits for
+  // its own copies of tile kt + 1 (those of kt + 2 may stay in flight), then
+  // the barrier makes every share visible and frees the stage of tile kt - 1,
+  // which tile kt + 3 now fills.
+  static_assert(kDqStages == 4, "wait counts below assume four stages");
   constexpr int kLoadsPerTile = 2 * Tile::NJ;
-  // Tiles [0, nkt_u) need no mask for any row of the workgroup.
-  const int nkt_u = CAUSAL ? min(nkt, q0 / kTileRows)
-                           : (len % kTileRows == 0 ? nkt : nkt - 1);
-  int kt = 0, st = 0;
+  int kt = 0;
   auto sync = [&]() __attribute__((always_inline)) {
-    if (kt + 1 < nkt)
+    if (kt + 2 < nkt)
       wait_vm_upto<kLoadsPerTile>();
     else
       wait_vm_all();
     __syncthreads();
-    if (kt + 2 < nkt) issue(kt + 2, st == 0 ? 2 : st - 1);
+    if (kt + 3 < nkt) issue(kt + 3);
   };
-  auto advance = [&]() __attribute__((always_inline)) {
-    st = st == kDqStages - 1 ? 0 : st + 1;
+  // Tiles [0, nun) need no mask and run pipelined: the S^T registers
+  // alternate between two sets, `r` selecting the one holding tile kt, so
+  // that the loop needs no register copies.  The remaining tiles of this
+  // wavefront (at the causal diagonal or the sequence end) run one at a time.
+  const int nun = min(nkt_u, nkt_w);
+  f32x16 s0, s1;
+  auto step = [&](auto r, auto next) __attribute__((always_inline)) {
+    f32x16& sc = decltype(r)::value ? s1 : s0;
+    f32x16& sn = decltype(r)::value ? s0 : s1;
+    sync();
+    f32x16 dp;
+    u32x4 b[2];
+    score(vptr(kt), doreg, dp);
+    softmax(kt, sc, std::false_type{});
+    if constexpr (decltype(next)::value) score(kptr(kt + 1), qreg, sn);
+    dscore(sc, dp, b);
+    accum(kt, b);
     ++kt;
   };
-  if (nkt > 0) issue(0, 0);
-  if (nkt > 1) issue(1, 1);
-  while (kt < nkt_u) {
-    sync();
-    compute(kt, st, std::false_type{});
-    advance();
+  using T = std::true_type;
+  using F = std::false_type;
+  // Tile 0 is visible (first prologue barrier).
+  if (nun > 0) score(kptr(0), qreg, s0);
+  while (kt + 2 < nun) {
+    step(F{}, T{});
+    step(T{}, T{});
+  }
+  if (kt + 2 == nun) {
+    step(F{}, T{});
+    step(T{}, F{});
+  } else if (kt + 1 == nun) {
+    step(F{}, F{});
   }
   while (kt < nkt_w) {
     sync();
-    compute(kt, st, std::true_type{});
-    advance();
+    f32x16 dp;
+    u32x4 b[2];
+    score(kptr(kt), qreg, s0);
+    score(vptr(kt), doreg, dp);
+    softmax(kt, s0, std::true_type{});
+    dscore(s0, dp, b);
+    accum(kt, b);
+    ++kt;
   }
   while (kt < nkt) {   // fully masked for this wavefront: loads only
     sync();
-    advance();
+    ++kt;
   }
 
-  // Add the two partial accumulators of each row through LDS.
+  // Add the two partial accumulators of each row through LDS.  The pair
+  // splits the columns: the kb = 0 wavefront finalises d < D/2, the kb = 1
+  // one the rest.  Each hands its partial of the other half to its partner,
+  // adds the partner's partial to its own half, stages the bf16 half-rows in
+  // LDS and writes them out as whole half-rows (coalesced 16-byte stores).
   __syncthreads();
   u32x4* const red = reinterpret_cast<u32x4*>(smem);
-  if (kb == 1) {
+  constexpr int H = D / 64;   // 32-column blocks per half
+  constexpr int HS = H * 4;   // u32x4 slots per lane for one half
+  auto hand = [&](auto lo) __attribute__((always_inline)) {
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db)
+    for (int i = 0; i < H; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        red[(qg * SM::RED_SLOTS + 4 * db + j) * 64 + lane] =
+      for (int j = 0; j < 4; ++j) {
+        const int db = decltype(lo)::value + i;
+        red[(wave * HS + 4 * i + j) * 64 + lane] =
             u32x4{__float_as_uint(dqacc[db][4 * j]), __float_as_uint(dqacc[db][4 * j + 1]),
                   __float_as_uint(dqacc[db][4 * j + 2]), __float_as_uint(dqacc[db][4 * j + 3])};
-  }
+      }
+  };
+  if (kb == 0)
+    hand(std::integral_constant<int, H>{});
+  else
+    hand(std::integral_constant<int, 0>{});
   __syncthreads();
-  if (kb == 1 || !valid) return;
-  uint16_t* dqp = a.dq + qoff + (int64_t)qrow * L.q_row;
+  auto finalize = [&](auto lo) __attribute__((always_inline)) {
+    constexpr int db0 = decltype(lo)::value;
+    const u32x4* src = red + (wave ^ 4) * HS * 64;
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db)
+    for (int i = 0; i < H; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const u32x4 pq = red[(qg * SM::RED_SLOTS + 4 * db + j) * 64 + lane];
-      float v[4];
+      for (int j = 0; j < 4; ++j) {
+        const u32x4 pp = src[(4 * i + j) * 64 + lane];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = (dqacc[db][4 * j + i] + __uint_as_float(pq[i])) * a.scale;
-      st8(dqp + 32 * db + 8 * j + 4 * half, u32x2{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])});
+        for (int e = 0; e < 4; ++e)
+          dqacc[db0 + i][4 * j + e] = (dqacc[db0 + i][4 * j + e] + __uint_as_float(pp[e])) * a.scale;
+      }
+    // Stage [32 rows][D/2] bf16 in the partner's region (read above); the
+    // 16-byte chunks of a half-row are swizzled by the row's low bits.
+    constexpr int CPR = D / 16;   // chunks per half-row
+    uint16_t* stg = reinterpret_cast<uint16_t*>(red + (wave ^ 4) * HS * 64);
+    const int sw = l32 & (CPR - 1);
+#pragma unroll
+    for (int i = 0; i < H; ++i)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x16& v = dqacc[db0 + i];
+        st8(stg + l32 * (D / 2) + 8 * ((4 * i + g) ^ sw) + 4 * half,
+            u32x2{pack_bf16(v[4 * g], v[4 * g + 1]), pack_bf16(v[4 * g + 2], v[4 * g + 3])});
+      }
+    uint16_t* const dqp = a.dq + qoff + 32 * db0;
+#pragma unroll
+    for (int i = 0; i < 32 * CPR / 64; ++i) {
+      const int pidx = i * 64 + lane;
+      const int row = pidx / CPR, ch = pidx % CPR;
+      const u32x4 v = ld16(stg + row * (D / 2) + 8 * (ch ^ (row & (CPR - 1))));
+      if (qw0 + row < len) st16(dqp + (int64_t)(qw0 + row) * L.q_row + 8 * ch, v);
     }
+  };
+  if (kb == 0)
+    finalize(std::integral_constant<int, 0>{});
+  else
+    finalize(std::integral_constant<int, H>{});
 }
 
 // ---------------------------------------------------------------------------
@@ -287,9 +389,8 @@ struct DkvSmem {
   static constexpr int LSE = DO + 2 * TILE;                // 2 stages x 64 fp32
   static constexpr int DEL = LSE + 2 * 256;
   static constexpr int BYTES = DEL + 2 * 256;
-  // partial dK/dV of wavefronts 4..7: (D/32) x 2 f32x16 per lane
-  static constexpr int RED_SLOTS = (D / 32) * 2 * 4;       // u32x4 slots per lane
-  static_assert(4 * RED_SLOTS * 1024 <= BYTES, "reduction buffer");
+  // epilogue: one tensor's partial per wavefront, (D/32) x 4 u32x4 per lane
+  static_assert(8 * (D / 32) * 4 * 1024 <= BYTES, "reduction buffer");
 };
 
 template <int D, bool CAUSAL>
@@ -457,39 +558,62 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
     for (; n < nend; ++n) step(n, std::false_type{});
   }
 
-  // Add the two partial accumulators of each key through LDS.
+  // Add the two partial accumulators of each key through LDS.  The pair
+  // splits the work: the sb = 0 wavefront finalises dK, the sb = 1 one dV.
+  // Each first hands its partial of the other tensor to its partner, then
+  // adds the partner's partial to its own, stages the bf16 rows in LDS and
+  // writes them out as whole rows (coalesced 16-byte stores).
   __syncthreads();
   u32x4* const red = reinterpret_cast<u32x4*>(smem);
-  if (sb == 1) {
+  constexpr int SL = (D / 32) * 4;   // u32x4 slots per lane for one tensor
+  auto hand = [&](const f32x16 (&acc)[D / 32]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        red[(wave * SL + 4 * db + j) * 64 + lane] =
+            u32x4{__float_as_uint(acc[db][4 * j]), __float_as_uint(acc[db][4 * j + 1]),
+                  __float_as_uint(acc[db][4 * j + 2]), __float_as_uint(acc[db][4 * j + 3])};
+  };
+  if (sb == 0)
+    hand(dvacc);
+  else
+    hand(dkacc);
+  __syncthreads();
+  const int64_t kv_row = L.kv_row;
+  auto finalize = [&](f32x16 (&acc)[D / 32], float mul, uint16_t* gout) __attribute__((always_inline)) {
+    const u32x4* src = red + (wave ^ 4) * SL * 64;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int slot = (kq * SM::RED_SLOTS + (2 * db) * 4 + j) * 64 + lane;
-        red[slot] = u32x4{__float_as_uint(dkacc[db][4 * j]), __float_as_uint(dkacc[db][4 * j + 1]),
-                          __float_as_uint(dkacc[db][4 * j + 2]), __float_as_uint(dkacc[db][4 * j + 3])};
-        red[slot + 4 * 64] = u32x4{__float_as_uint(dvacc[db][4 * j]), __float_as_uint(dvacc[db][4 * j + 1]),
-                                   __float_as_uint(dvacc[db][4 * j + 2]), __float_as_uint(dvacc[db][4 * j + 3])};
+        const u32x4 pp = src[(4 * db + j) * 64 + lane];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[db][4 * j + i] = (acc[db][4 * j + i] + __uint_as_float(pp[i])) * mul;
       }
-  }
-  __syncthreads();
-  if (sb == 1 || krow >= len) return;
-  const int64_t off = kvoff + (int64_t)krow * L.kv_row;
+    // Stage [32 keys][D] bf16 in the partner's region (read above), 16-byte
+    // chunks swizzled by row as in the tiles.
+    uint16_t* stg = reinterpret_cast<uint16_t*>(red + (wave ^ 4) * SL * 64);
+    const int sw = tile_swz<D>(l32);
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db)
+    for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int slot = (kq * SM::RED_SLOTS + (2 * db) * 4 + j) * 64 + lane;
-      const u32x4 pk = red[slot], pv = red[slot + 4 * 64];
-      float dk[4], dv[4];
+      for (int g = 0; g < 4; ++g)
+        st8(stg + l32 * D + 8 * ((4 * db + g) ^ sw) + 4 * half,
+            u32x2{pack_bf16(acc[db][4 * g], acc[db][4 * g + 1]), pack_bf16(acc[db][4 * g + 2], acc[db][4 * g + 3])});
+    constexpr int CPR = D / 8;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        dk[i] = (dkacc[db][4 * j + i] + __uint_as_float(pk[i])) * a.scale;
-        dv[i] = dvacc[db][4 * j + i] + __uint_as_float(pv[i]);
-      }
-      st8(a.dk + off + 32 * db + 8 * j + 4 * half, u32x2{pack_bf16(dk[0], dk[1]), pack_bf16(dk[2], dk[3])});
-      st8(a.dv + off + 32 * db + 8 * j + 4 * half, u32x2{pack_bf16(dv[0], dv[1]), pack_bf16(dv[2], dv[3])});
+    for (int i = 0; i < 32 * CPR / 64; ++i) {
+      const int pidx = i * 64 + lane;
+      const int row = pidx / CPR, ch = pidx % CPR;
+      const u32x4 v = ld16(stg + row * D + 8 * (ch ^ tile_swz<D>(row)));
+      if (kw0 + row < len) st16(gout + (int64_t)(kw0 + row) * kv_row + 8 * ch, v);
     }
+  };
+  if (sb == 0)
+    finalize(dkacc, a.scale, a.dk + kvoff);
+  else
+    finalize(dvacc, 1.f, a.dv + kvoff);
 }
 
 // Explicit instantiations: without them the host compiler may skip the

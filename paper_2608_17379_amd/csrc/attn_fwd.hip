@@ -5,12 +5,13 @@
 // exp(m_old - m_new) when the maximum moves, and normalise by l in the
 // epilogue, where L = m + log l.
 //
-// Work split: one workgroup of 4 wavefronts per (segment, query head, 128
-// query rows); each wavefront owns 32 query rows.  The wavefront computes the
-// transposed score tile S^T = K Q^T on MFMA, so lane l holds every score of
-// query (l % 32) against half of the tile's keys: the row maximum and row sum
-// are in-lane reductions plus one exchange with lane l ^ 32.  P^T, rounded to
-// bf16, is then already laid out as the B operand of O^T += V^T P^T.
+// Work split: one workgroup of 4 wavefronts per (segment, query head, pair of
+// 128-row query blocks), two workgroups per CU; each wavefront owns 32 query
+// rows.  The wavefront computes the transposed score tile S^T = K Q^T on
+// MFMA, so lane l holds every score of query (l % 32) against half of the
+// tile's keys: the row maximum and row sum are in-lane reductions plus one
+// exchange with lane l ^ 32.  P^T, rounded to bf16, is then already laid out
+// as the B operand of O^T += V^T P^T.
 //
 // The reference maximum used for P is only moved when a tile's row maximum
 // exceeds it by more than 2^8 (in exp2 units), so most tiles skip the
@@ -54,170 +55,182 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   const int z = blockIdx.x / L.Hq, h = blockIdx.x % L.Hq;
   const int hk = h / L.group;
   const Segment seg = segment_of(L, z);
-  const int qt = (int)gridDim.y - 1 - (int)blockIdx.y;  // longest rows first
-  const int q0 = qt * kBM;
-  if (q0 >= seg.len) return;
+  // Query blocks nqt - 1 - p and p of the segment, in that order: under the
+  // causal mask every workgroup then has the same number of key tiles, so the
+  // two workgroups sharing a CU finish together.
+  const int nqt = (seg.len + kBM - 1) / kBM;
+  const int p = (int)blockIdx.y;
+  if (p > nqt - 1 - p) return;
 
-  const int64_t qoff = (int64_t)seg.start * L.q_row + (int64_t)z * L.q_batch +
-                       (int64_t)h * L.q_head;
-  const int64_t kvoff = (int64_t)seg.start * L.kv_row + (int64_t)z * L.kv_batch +
-                        (int64_t)hk * L.kv_head;
-  const int64_t roff = (int64_t)seg.start + (int64_t)z * L.r_batch + (int64_t)h * L.r_head;
-  const uint16_t* kp = a.k + kvoff;
-  const uint16_t* vp = a.v + kvoff;
+#pragma nounroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int qt = pass == 0 ? nqt - 1 - p : p;
+    if (pass == 1) {
+      if (qt >= nqt - 1 - p) break;
+      __syncthreads();   // the first block's last tile is read before stage 0 refills
+    }
+    const int q0 = qt * kBM;
+    const int64_t qoff = (int64_t)seg.start * L.q_row + (int64_t)z * L.q_batch +
+                         (int64_t)h * L.q_head;
+    const int64_t kvoff = (int64_t)seg.start * L.kv_row + (int64_t)z * L.kv_batch +
+                          (int64_t)hk * L.kv_head;
+    const int64_t roff = (int64_t)seg.start + (int64_t)z * L.r_batch + (int64_t)h * L.r_head;
+    const uint16_t* kp = a.k + kvoff;
+    const uint16_t* vp = a.v + kvoff;
 
-  // This lane's query row, held as B operands of S^T = K Q^T:
-  // qreg[c] = Q[qrow][16c + 8*half .. +8].
-  const int qw0 = q0 + wave * 32;
-  const int qrow = qw0 + l32;
-  u32x4 qreg[D / 16];
-  {
-    const rsrc_t rq = rows_rsrc(a.q + qoff, qw0, seg.len, L.q_row);
-    const int base = l32 * (int)(L.q_row * 2) + 16 * half;
+    // This lane's query row, held as B operands of S^T = K Q^T:
+    // qreg[c] = Q[qrow][16c + 8*half .. +8].
+    const int qw0 = q0 + wave * 32;
+    const int qrow = qw0 + l32;
+    u32x4 qreg[D / 16];
+    {
+      const rsrc_t rq = rows_rsrc(a.q + qoff, qw0, seg.len, L.q_row);
+      const int base = l32 * (int)(L.q_row * 2) + 16 * half;
 #pragma unroll
-    for (int c = 0; c < D / 16; ++c) qreg[c] = bload16(rq, base + 32 * c);
-  }
+      for (int c = 0; c < D / 16; ++c) qreg[c] = bload16(rq, base + 32 * c);
+    }
 
-  const int kend = a.causal ? min(seg.len, q0 + kBM) : seg.len;
-  const int nkt = (kend + kBN - 1) / kBN;
+    const int kend = a.causal ? min(seg.len, q0 + kBM) : seg.len;
+    const int nkt = (kend + kBN - 1) / kBN;
 
-  const Tile dma(wave, lane, (int)(L.kv_row * 2));
-  const RowReader<D> kr(l32, half);
-  const TransReader<D> vr(lane);
+    const Tile dma(wave, lane, (int)(L.kv_row * 2));
+    const RowReader<D> kr(l32, half);
+    const TransReader<D> vr(lane);
 
-  f32x16 oacc[D / 32];
+    f32x16 oacc[D / 32];
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db)
+    for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
-  float mref = -INFINITY;   // reference max of scale*log2(e)*s for query qrow
-  float lsum = 0.f;         // this lane's share of the row sum, relative to mref
-  const float sl2 = a.scale_log2;
-  // Fields used inside the lambdas below, as plain values (capturing the
-  // kernel argument itself can make the compiler spill it to scratch).
-  const bool causal = a.causal != 0;
-  const int len = seg.len;
-  const int64_t kv_row = L.kv_row;
+      for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
+    float mref = -INFINITY;   // reference max of scale*log2(e)*s for query qrow
+    float lsum = 0.f;         // this lane's share of the row sum, relative to mref
+    const float sl2 = a.scale_log2;
+    // Fields used inside the lambdas below, as plain values (capturing the
+    // kernel argument itself can make the compiler spill it to scratch).
+    const bool causal = a.causal != 0;
+    const int len = seg.len;
+    const int64_t kv_row = L.kv_row;
 
-  auto compute = [&](int kt, const uint16_t* kt_lds, const uint16_t* vt_lds) __attribute__((always_inline)) {
-    const int k0 = kt * kBN;
-    f32x16 s[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
-#pragma unroll
-    for (int c = 0; c < D / 16; ++c)
+    auto compute = [&](int kt, const uint16_t* kt_lds, const uint16_t* vt_lds) __attribute__((always_inline)) {
+      const int k0 = kt * kBN;
+      f32x16 s[2];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
-        s[kb] = mfma32(ld16(kt_lds + kr.rm[c] + 32 * kb * D), qreg[c], s[kb]);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+#pragma unroll
+      for (int c = 0; c < D / 16; ++c)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+          s[kb] = mfma32(ld16(kt_lds + kr.rm[c] + 32 * kb * D), qreg[c], s[kb]);
 
-    // s[kb][r] is the raw score of key k0 + 32kb + 8(r/4) + 4half + r%4.
-    if ((a.causal && k0 + kBN - 1 > qw0) || k0 + kBN > seg.len) {
+      // s[kb][r] is the raw score of key k0 + 32kb + 8(r/4) + 4half + r%4.
+      if ((a.causal && k0 + kBN - 1 > qw0) || k0 + kBN > seg.len) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = k0 + 32 * kb + 8 * (r / 4) + 4 * half + (r % 4);
+            const bool masked = (a.causal && key > qrow) || key >= seg.len;
+            s[kb][r] = masked ? -INFINITY : s[kb][r];
+          }
+      }
+      float mx = s[0][0];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
+      mx = fmaxf(mx, swap_halves(mx));
+      const float mt = mx * sl2;   // this tile's row max in exp2 units
+      if (__ballot(mt > mref + kRescaleSlack)) {
+        const float mnew = fmaxf(mref, mt);
+        const float alpha = fast_exp2(mref - mnew);   // 0 on the first visible tile
+        lsum *= alpha;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+        mref = mnew;
+      }
+      const float mneg = mref == -INFINITY ? 0.f : -mref;
+      float rs = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = k0 + 32 * kb + 8 * (r / 4) + 4 * half + (r % 4);
-          const bool masked = (a.causal && key > qrow) || key >= seg.len;
-          s[kb][r] = masked ? -INFINITY : s[kb][r];
+          const float pe = fast_exp2(__builtin_fmaf(s[kb][r], sl2, mneg));
+          s[kb][r] = pe;
+          rs += pe;
         }
+      lsum += rs;
+
+      // O^T[d][q] += sum_key V^T[d][key] P^T[key][q]; chunk c = keys 16c..16c+15,
+      // V^T read transposed out of the row-major V tile.
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const u32x4 pb = pack_chunk(s[c >> 1], c & 1);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          const u32x2 lo = ld_tr(vt_lds + vr.tr[db][0] + 16 * c * D);
+          const u32x2 hi = ld_tr(vt_lds + vr.tr[db][1] + 16 * c * D);
+          oacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb, oacc[db]);
+        }
+      }
+    };
+    // One tile: wait for its loads (this wavefront's, then everyone's through
+    // the barrier, which also frees the stage read one tile earlier), start the
+    // next tile's loads into that stage, then compute.
+    auto step = [&](int kt, bool work, const uint16_t* kc, const uint16_t* vc, uint16_t* kn,
+                    uint16_t* vn) __attribute__((always_inline)) {
+      wait_vm<0>();
+      __syncthreads();
+      if (kt + 1 < nkt) {
+        dma.load(rows_rsrc(kp, (kt + 1) * kBN, len, kv_row), kn, wave);
+        dma.load(rows_rsrc(vp, (kt + 1) * kBN, len, kv_row), vn, wave);
+      }
+      if (work) compute(kt, kc, vc);
+    };
+
+    // Tiles past this wavefront's last query are fully masked for it: the
+    // wavefront only joins their barriers and loads.
+    const int nkt_w = causal ? min(nkt, (qw0 + 31) / kBN + 1) : nkt;
+    if (nkt > 0) {
+      dma.load(rows_rsrc(kp, 0, seg.len, L.kv_row), sk0, wave);
+      dma.load(rows_rsrc(vp, 0, seg.len, L.kv_row), sv0, wave);
     }
-    float mx = s[0][0];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-    mx = fmaxf(mx, swap_halves(mx));
-    const float mt = mx * sl2;   // this tile's row max in exp2 units
-    if (__ballot(mt > mref + kRescaleSlack)) {
-      const float mnew = fmaxf(mref, mt);
-      const float alpha = fast_exp2(mref - mnew);   // 0 on the first visible tile
-      lsum *= alpha;
+    wait_vm<0>();   // Q rows and the first tile
+    int kt = 0;
+    for (; kt + 1 < nkt_w; kt += 2) {
+      step(kt, true, sk0, sv0, sk1, sv1);
+      step(kt + 1, true, sk1, sv1, sk0, sv0);
+    }
+    if (kt < nkt_w) {
+      step(kt, true, sk0, sv0, sk1, sv1);
+      ++kt;
+    }
+    for (; kt < nkt; ++kt) {
+      if (kt & 1)
+        step(kt, false, sk1, sv1, sk0, sv0);
+      else
+        step(kt, false, sk0, sv0, sk1, sv1);
+    }
+
+    // Epilogue: O = O / l, L = (m + log2 l) ln 2.
+    lsum += swap_halves(lsum);
+    if (qrow < seg.len) {
+      const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+      uint16_t* op = a.o + qoff + (int64_t)qrow * L.q_row;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
-      mref = mnew;
+        for (int g = 0; g < 4; ++g) {
+          u32x2 w;
+          w[0] = pack_bf16(oacc[db][4 * g + 0] * inv, oacc[db][4 * g + 1] * inv);
+          w[1] = pack_bf16(oacc[db][4 * g + 2] * inv, oacc[db][4 * g + 3] * inv);
+          st8(op + 32 * db + 8 * g + 4 * half, w);
+        }
+      if (half == 0) a.lse[roff + qrow] = lsum > 0.f ? (mref + log2f(lsum)) * kLn2 : -INFINITY;
     }
-    const float mneg = mref == -INFINITY ? 0.f : -mref;
-    float rs = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = fast_exp2(__builtin_fmaf(s[kb][r], sl2, mneg));
-        s[kb][r] = p;
-        rs += p;
-      }
-    lsum += rs;
-
-    // O^T[d][q] += sum_key V^T[d][key] P^T[key][q]; chunk c = keys 16c..16c+15,
-    // V^T read transposed out of the row-major V tile.
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const u32x4 pb = pack_chunk(s[c >> 1], c & 1);
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
-        const u32x2 lo = ld_tr(vt_lds + vr.tr[db][0] + 16 * c * D);
-        const u32x2 hi = ld_tr(vt_lds + vr.tr[db][1] + 16 * c * D);
-        oacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb, oacc[db]);
-      }
-    }
-  };
-  // One tile: wait for its loads (this wavefront's, then everyone's through
-  // the barrier, which also frees the stage read one tile earlier), start the
-  // next tile's loads into that stage, then compute.
-  auto step = [&](int kt, bool work, const uint16_t* kc, const uint16_t* vc, uint16_t* kn,
-                  uint16_t* vn) __attribute__((always_inline)) {
-    wait_vm<0>();
-    __syncthreads();
-    if (kt + 1 < nkt) {
-      dma.load(rows_rsrc(kp, (kt + 1) * kBN, len, kv_row), kn, wave);
-      dma.load(rows_rsrc(vp, (kt + 1) * kBN, len, kv_row), vn, wave);
-    }
-    if (work) compute(kt, kc, vc);
-  };
-
-  // Tiles past this wavefront's last query are fully masked for it: the
-  // wavefront only joins their barriers and loads.
-  const int nkt_w = causal ? min(nkt, (qw0 + 31) / kBN + 1) : nkt;
-  if (nkt > 0) {
-    dma.load(rows_rsrc(kp, 0, seg.len, L.kv_row), sk0, wave);
-    dma.load(rows_rsrc(vp, 0, seg.len, L.kv_row), sv0, wave);
-  }
-  wait_vm<0>();   // Q rows and the first tile
-  int kt = 0;
-  for (; kt + 1 < nkt_w; kt += 2) {
-    step(kt, true, sk0, sv0, sk1, sv1);
-    step(kt + 1, true, sk1, sv1, sk0, sv0);
-  }
-  if (kt < nkt_w) {
-    step(kt, true, sk0, sv0, sk1, sv1);
-    ++kt;
-  }
-  for (; kt < nkt; ++kt) {
-    if (kt & 1)
-      step(kt, false, sk1, sv1, sk0, sv0);
-    else
-      step(kt, false, sk0, sv0, sk1, sv1);
-  }
-
-  // Epilogue: O = O / l, L = (m + log2 l) ln 2.
-  lsum += swap_halves(lsum);
-  if (qrow < seg.len) {
-    const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
-    uint16_t* op = a.o + qoff + (int64_t)qrow * L.q_row;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        u32x2 w;
-        w[0] = pack_bf16(oacc[db][4 * g + 0] * inv, oacc[db][4 * g + 1] * inv);
-        w[1] = pack_bf16(oacc[db][4 * g + 2] * inv, oacc[db][4 * g + 3] * inv);
-        st8(op + 32 * db + 8 * g + 4 * half, w);
-      }
-    if (half == 0) a.lse[roff + qrow] = lsum > 0.f ? (mref + log2f(lsum)) * kLn2 : -INFINITY;
   }
 }
 
@@ -229,7 +242,9 @@ template __global__ void fwd_kernel<128>(FwdArgs);
 }  // namespace
 
 hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream) {
-  const dim3 grid((unsigned)(a.L.nseg * a.L.Hq), (unsigned)((a.L.S + kBM - 1) / kBM));
+  // Each workgroup takes a query block and its mirror (see the kernel).
+  const int nqt = (a.L.S + kBM - 1) / kBM;
+  const dim3 grid((unsigned)(a.L.nseg * a.L.Hq), (unsigned)((nqt + 1) / 2));
   if (D == 64)
     hipLaunchKernelGGL(fwd_kernel<64>, grid, dim3(kThreads), 0, stream, a);
   else

@@ -8,22 +8,23 @@
 // (the backward workloads of PTXBench, Appendix A, consume Q, K, V, O, dO and
 // L and return dQ, dK, dV).  Two kernels, both free of atomics:
 //
-//  * bwd_dq_kernel: one workgroup per (segment, query head, 128 query rows),
-//    32 rows per wavefront.  Its prologue computes Delta for its rows (the
-//    rows' dO and O are read once) and stores it in the workspace; the loop
-//    over key tiles recomputes S^T = K Q^T and dP^T = V dO^T, forms dS^T in
+//  * bwd_dq_kernel: one workgroup of 4 wavefronts per (segment, query head,
+//    128-row query block and its causal mirror), 32 rows per wavefront, two
+//    workgroups per CU.  Its prologue computes Delta for its rows (the rows'
+//    dO and O are read once) and stores it in the workspace; the loop over
+//    key tiles recomputes S^T = K Q^T and dP^T = V dO^T, forms dS^T in
 //    registers and accumulates dQ^T += K^T dS^T.
-//  * bwd_dkdv_kernel: one workgroup per (segment, key/value head, 128 keys),
-//    32 keys per wavefront, launched after bwd_dq_kernel (it reads Delta).
-//    The wavefront keeps its K and V rows in registers and loops over every
-//    query head of the group and every query tile that can see its keys,
-//    accumulating dV^T += dO^T P and dK^T += Q^T dS in registers; the
-//    grouped-query sum therefore needs no cross-workgroup reduction.
+//  * bwd_dkdv_kernel: one workgroup of 8 wavefronts per (segment, key/value
+//    head, 128 keys), launched after bwd_dq_kernel (it reads Delta).  The
+//    workgroup keeps its K and V rows in LDS and loops over every query head
+//    of the group and every query tile that can see its keys, accumulating
+//    dV^T += dO^T P and dK^T += Q^T dS in registers; the grouped-query sum
+//    therefore needs no cross-workgroup reduction.
 //
 // Tiles of 64 rows (K and V for dQ; Q, dO, L and Delta for dK/dV) go from
-// global memory straight into two LDS stages (buffer_load ... lds, bounded
-// at the segment end so that rows past it read as zero), issued a tile ahead
-// with one barrier per tile.  They stay row-major in LDS: operands whose
+// global memory straight into a ring of LDS stages (buffer_load ... lds,
+// bounded at the segment end so that rows past it read as zero), issued a
+// tile ahead with one barrier per tile.  They stay row-major in LDS: operands whose
 // reduction index runs along the tile's rows (K^T, Q^T, dO^T) come out of the
 // same tiles through the transposing read ds_read_b64_tr_b16.  Accumulator
 // tiles are fed back as B operands directly (device_common.hpp).
@@ -44,31 +45,30 @@ constexpr int kTileRows = 64;
 // ---------------------------------------------------------------------------
 // dQ (and Delta)
 //
-// Eight wavefronts per workgroup of 128 query rows: wavefronts w and w + 4
-// (which share a SIMD) own the same 32 rows and take the two 32-key halves of
-// every 64-key tile, so each SIMD runs two independent wavefronts.  K and V
-// tiles stream through a four-stage LDS ring; the two partial dQ accumulators of
-// each row are added through LDS at the end.
+// Four wavefronts per workgroup of 128 query rows, 32 rows each, and two
+// workgroups per CU (within 256 VGPRs per wavefront and 64 KiB of LDS per
+// workgroup): the two wavefronts on a SIMD belong to different workgroups,
+// so no common barrier holds them in step, and one workgroup's prologue and
+// epilogue run under the other's loop.  K and V tiles stream through two
+// LDS stages; each wavefront takes both 32-key halves of every tile.  A
+// workgroup takes a query block and its causal mirror, so that every
+// workgroup has the same number of key tiles.
 // ---------------------------------------------------------------------------
 constexpr int kQM = 128;   // query rows per workgroup
-constexpr int kDqWaves = 8;
+constexpr int kDqWaves = 4;
 constexpr int kDqThreads = 64 * kDqWaves;
-
-constexpr int kDqStages = 4;   // K/V ring depth (a power of two)
 
 template <int D>
 struct DqSmem {
-  static constexpr int TILE = 64 * D * 2;                  // bytes of a 64-row bf16 tile
-  static constexpr int K = 0;                              // kDqStages stages
-  static constexpr int V = K + kDqStages * TILE;           // kDqStages stages
-  static constexpr int X = V + kDqStages * TILE;           // 2 tiles, used by the prologue
-  static constexpr int BYTES = X + 2 * TILE;
-  // epilogue: half of a dQ partial per wavefront, (D/64) x 4 u32x4 per lane
-  static_assert(8 * (D / 64) * 4 * 1024 <= BYTES, "reduction buffer");
+  static constexpr int TILE = 64 * D * 2;   // bytes of a 64-row bf16 tile
+  static constexpr int K = 0;               // 2 stages
+  static constexpr int V = K + 2 * TILE;    // 2 stages
+  static constexpr int BYTES = V + 2 * TILE;
+  static_assert(kDqWaves * 32 * D * 2 <= BYTES, "epilogue staging");
 };
 
 template <int D, bool CAUSAL>
-__global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdArgs a) {
+__global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
   using Tile = AsyncTile<D, kDqWaves>;
   using SM = DqSmem<D>;
   __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
@@ -76,292 +76,203 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = wave_id();
   const int l32 = lane & 31, half = lane >> 5;
-  const int qg = wave & 3;    // 32-row group
-  const int kb = wave >> 2;   // which 32-key half of each tile
 
   const Layout L = a.L;
   const int z = blockIdx.x / L.Hq, h = blockIdx.x % L.Hq;
   const int hk = h / L.group;
   const Segment seg = segment_of(L, z);
-  const int qt = (int)gridDim.y - 1 - (int)blockIdx.y;
-  const int q0 = qt * kQM;
-  if (q0 >= seg.len) return;
+  const int nqt = (seg.len + kQM - 1) / kQM;
+  const int p = (int)blockIdx.y;
+  if (p > nqt - 1 - p) return;
 
-  const int64_t qoff = (int64_t)seg.start * L.q_row + (int64_t)z * L.q_batch +
-                       (int64_t)h * L.q_head;
-  const int64_t kvoff = (int64_t)seg.start * L.kv_row + (int64_t)z * L.kv_batch +
-                        (int64_t)hk * L.kv_head;
-  const int64_t roff = (int64_t)seg.start + (int64_t)z * L.r_batch + (int64_t)h * L.r_head;
-  const uint16_t* const kp = a.k + kvoff;
-  const uint16_t* const vp = a.v + kvoff;
-  const int64_t kv_row_b = L.kv_row * 2;
+  // Fields used inside the lambdas below, as plain values (capturing the
+  // kernel argument itself would make the compiler spill it to scratch).
   const int len = seg.len;
   const float sl2 = a.scale_log2;
-
-  const int qw0 = q0 + qg * 32;
-  const int qrow = qw0 + l32;
-  const bool valid = qrow < len;
-
-  const int kend = CAUSAL ? min(len, q0 + kQM) : len;
-  const int nkt = (kend + kTileRows - 1) / kTileRows;
-  // Key tiles whose keys in this wavefront's half all follow its last row
-  // are fully masked for it.
-  const int nkt_w = CAUSAL ? min(nkt, (qw0 + 31 - 32 * kb) / kTileRows + 1) : nkt;
-  // Tiles [0, nkt_u) need no mask for any row of the workgroup.
-  const int nkt_u = CAUSAL ? min(nkt, q0 / kTileRows)
-                           : (len % kTileRows == 0 ? nkt : nkt - 1);
-
-  const Tile dma(wave, lane, (int)kv_row_b);
+  const float scale = a.scale;
+  const int64_t kv_row_b = L.kv_row * 2;
+  const int64_t q_row = L.q_row;
   const uint32_t sbase = lds_addr(smem);
-  auto issue = [&](int kt) __attribute__((always_inline)) {
-    const int st = kt & (kDqStages - 1);
-    dma_tile<D>(dma, rows_desc(kp, kt * kTileRows, len, kv_row_b), sbase + SM::K + st * SM::TILE,
-                wave);
-    dma_tile<D>(dma, rows_desc(vp, kt * kTileRows, len, kv_row_b), sbase + SM::V + st * SM::TILE,
-                wave);
-  };
+  const Tile dma(wave, lane, (int)kv_row_b);
   const RowReader<D> rr(l32, half);
-
-  // Prologue: the workgroup's Q, dO and O rows go through LDS (one coalesced
-  // copy of each row instead of strided per-lane loads, repeated by both
-  // wavefronts of a pair), beside the first two K/V tiles.  The 64-row
-  // halves sit in the extra region (Q) and in stages 2 and 3 (dO, O), which
-  // the ring fills only after the rows have been read.
-  {
-    const Tile qdma(wave, lane, (int)(L.q_row * 2));
-    const int64_t q_row_b = L.q_row * 2;
-    auto rows = [&](const uint16_t* base, uint32_t lo, uint32_t hi) __attribute__((always_inline)) {
-      dma_tile<D>(qdma, rows_desc(base + qoff, q0, len, q_row_b), sbase + lo, wave);
-      dma_tile<D>(qdma, rows_desc(base + qoff, q0 + kTileRows, len, q_row_b), sbase + hi, wave);
-    };
-    rows(a.q, SM::X, SM::X + SM::TILE);
-    rows(a.dout, SM::K + 2 * SM::TILE, SM::V + 2 * SM::TILE);
-    rows(a.o, SM::K + 3 * SM::TILE, SM::V + 3 * SM::TILE);
-  }
-  if (nkt > 0) issue(0);
-  if (nkt > 1) issue(1);
-  float lse2 = 0.f;
-  if (valid) lse2 = a.lse[roff + qrow] * kLog2e;
-  wait_vm_all();
-  __syncthreads();
-
-  // Q^T and dO^T as B operands (this wavefront's 32 rows, in 64-row half
-  // qg / 2); Delta from dO and O in the same layout (stored by the kb = 0
-  // wavefront of each pair).
-  u32x4 qreg[D / 16], doreg[D / 16];
-  float dsum = 0.f;
-  {
-    const int sub = 32 * (qg & 1) * D;
-    const uint16_t* qs = reinterpret_cast<const uint16_t*>(smem + SM::X + (qg >> 1) * SM::TILE);
-    const uint16_t* dos = reinterpret_cast<const uint16_t*>(smem + ((qg >> 1) ? SM::V : SM::K) + 2 * SM::TILE);
-    const uint16_t* os = reinterpret_cast<const uint16_t*>(smem + ((qg >> 1) ? SM::V : SM::K) + 3 * SM::TILE);
-#pragma unroll
-    for (int c = 0; c < D / 16; ++c) {
-      qreg[c] = ld16(qs + rr.rm[c] + sub);
-      doreg[c] = ld16(dos + rr.rm[c] + sub);
-      const u32x4 ov = ld16(os + rr.rm[c] + sub);
-#pragma unroll
-      for (int w = 0; w < 4; ++w)
-        dsum += bf16_lo(doreg[c][w]) * bf16_lo(ov[w]) + bf16_hi(doreg[c][w]) * bf16_hi(ov[w]);
-    }
-  }
-  __syncthreads();   // stages 2 and 3 are free for the ring
-  if (nkt > 2) issue(2);
-  const float delta = dsum + swap_halves(dsum);
-  if (valid && kb == 0 && half == 0) a.delta[roff + qrow] = delta;
-
   const TransReader<D> trr(lane);
 
-  f32x16 dqacc[D / 32];
-#pragma unroll
-  for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) dqacc[db][r] = 0.f;
-
-  // One tile of this wavefront's work (32 keys x 32 rows):
-  //   S^T = K Q^T and dP^T = V dO^T (MFMA);
-  //   P^T = exp2(s scale log2 e - L log2 e), masked only on tiles at the
-  //   causal diagonal or the sequence end, and dS^T = P^T (dP^T - Delta),
-  //   packed to bf16 (VALU);
-  //   dQ^T += K^T dS^T with K^T read transposed (MFMA).
-  // The loop is software-pipelined so that each wavefront's MFMAs run under
-  // its own VALU work: tile kt's exponentials are issued beside its dP^T
-  // product, and its dS^T beside the S^T product of tile kt + 1.
-  auto kptr = [&](int kt) __attribute__((always_inline)) {
-    return reinterpret_cast<const uint16_t*>(smem + SM::K + (kt & (kDqStages - 1)) * SM::TILE);
-  };
-  auto vptr = [&](int kt) __attribute__((always_inline)) {
-    return reinterpret_cast<const uint16_t*>(smem + SM::V + (kt & (kDqStages - 1)) * SM::TILE);
-  };
-  auto score = [&](const uint16_t* tile, const u32x4 (&b)[D / 16], f32x16& acc)
-      __attribute__((always_inline)) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-#pragma unroll
-    for (int c = 0; c < D / 16; ++c) acc = mfma32(ld16(tile + rr.rm[c] + 32 * kb * D), b[c], acc);
-  };
-  auto softmax = [&](int kt, f32x16& s, auto masked) __attribute__((always_inline)) {
-    // s[r]: key ks0 + 8(r/4) + 4half + r%4, query qrow.
-    const int ks0 = kt * kTileRows + 32 * kb;
-    const int t = ks0 + 4 * half - qrow;   // the lane's first key minus its query
-    const int u = ks0 + 4 * half - len;    // the lane's first key minus the end
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      float p = fast_exp2(__builtin_fmaf(s[r], sl2, -lse2));
-      if constexpr (decltype(masked)::value) {
-        const int off = 8 * (r / 4) + (r % 4);
-        if constexpr (CAUSAL) p = t + off > 0 ? 0.f : p;   // key after query
-        p = u + off >= 0 ? 0.f : p;                        // key past the end
-      }
-      s[r] = p;
+#pragma nounroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int qt = pass == 0 ? nqt - 1 - p : p;
+    if (pass == 1) {
+      if (qt >= nqt - 1 - p) break;
+      __syncthreads();   // the first block's epilogue reads are done before the ring refills
     }
-  };
-  auto dscore = [&](f32x16& p, const f32x16& dp, u32x4 (&b)[2]) __attribute__((always_inline)) {
+    const int q0 = qt * kQM;
+    const int64_t qoff = (int64_t)seg.start * L.q_row + (int64_t)z * L.q_batch +
+                         (int64_t)h * L.q_head;
+    const int64_t kvoff = (int64_t)seg.start * L.kv_row + (int64_t)z * L.kv_batch +
+                          (int64_t)hk * L.kv_head;
+    const int64_t roff = (int64_t)seg.start + (int64_t)z * L.r_batch + (int64_t)h * L.r_head;
+    const uint16_t* const kp = a.k + kvoff;
+    const uint16_t* const vp = a.v + kvoff;
+
+    const int qw0 = q0 + wave * 32;
+    const int qrow = qw0 + l32;
+    const bool valid = qrow < len;
+
+    const int kend = CAUSAL ? min(len, q0 + kQM) : len;
+    const int nkt = (kend + kTileRows - 1) / kTileRows;
+    auto issue = [&](int kt) __attribute__((always_inline)) {
+      const uint32_t st = (uint32_t)(kt & 1) * SM::TILE;
+      dma_tile<D>(dma, rows_desc(kp, kt * kTileRows, len, kv_row_b), sbase + SM::K + st, wave);
+      dma_tile<D>(dma, rows_desc(vp, kt * kTileRows, len, kv_row_b), sbase + SM::V + st, wave);
+    };
+    // Both stages are free: the first two tiles go out before the row loads.
+    issue(0);
+    if (nkt > 1) issue(1);
+
+    // Q^T and dO^T as B operands; Delta from dO and O in the same layout.
+    u32x4 qreg[D / 16], doreg[D / 16];
+    float dsum = 0.f, lse2 = 0.f;
+    {
+      const rsrc_t rq = rows_rsrc(a.q + qoff, qw0, len, q_row);
+      const rsrc_t rdo = rows_rsrc(a.dout + qoff, qw0, len, q_row);
+      const rsrc_t ro = rows_rsrc(a.o + qoff, qw0, len, q_row);
+      const int base = l32 * (int)(q_row * 2) + 16 * half;
+      u32x4 ov[D / 16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) p[r] = p[r] * (dp[r] - delta);
-    b[0] = pack_chunk(p, 0);
-    b[1] = pack_chunk(p, 1);
-  };
-  auto accum = [&](int kt, const u32x4 (&b)[2]) __attribute__((always_inline)) {
-    const uint16_t* kc = kptr(kt);
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int rc = 16 * (2 * kb + c) * D;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
-        const u32x2 lo = ld_tr(kc + trr.tr[db][0] + rc), hi = ld_tr(kc + trr.tr[db][1] + rc);
-        dqacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, b[c], dqacc[db]);
+      for (int c = 0; c < D / 16; ++c) {
+        qreg[c] = bload16(rq, base + 32 * c);
+        doreg[c] = bload16(rdo, base + 32 * c);
+        ov[c] = bload16(ro, base + 32 * c);
       }
+      if (valid) lse2 = a.lse[roff + qrow] * kLog2e;
+      // Every row load is in flight before the first use.
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int c = 0; c < D / 16; ++c)
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          dsum += bf16_lo(doreg[c][w]) * bf16_lo(ov[c][w]) + bf16_hi(doreg[c][w]) * bf16_hi(ov[c][w]);
     }
-  };
+    const float delta = dsum + swap_halves(dsum);
+    if (valid && half == 0) a.delta[roff + qrow] = delta;
 
-  // Ring of kDqStages stages.  At the top of tile kt this wavefront waits for
-  // its own copies of tile kt + 1 (those of kt + 2 may stay in flight), then
-  // the barrier makes every share visible and frees the stage of tile kt - 1,
-  // which tile kt + 3 now fills.
-  static_assert(kDqStages == 4, "wait counts below assume four stages");
-  constexpr int kLoadsPerTile = 2 * Tile::NJ;
-  int kt = 0;
-  auto sync = [&]() __attribute__((always_inline)) {
-    if (kt + 2 < nkt)
-      wait_vm_upto<kLoadsPerTile>();
-    else
-      wait_vm_all();
-    __syncthreads();
-    if (kt + 3 < nkt) issue(kt + 3);
-  };
-  // Tiles [0, nun) need no mask and run pipelined: the S^T registers
-  // alternate between two sets, `r` selecting the one holding tile kt, so
-  // that the loop needs no register copies.  The remaining tiles of this
-  // wavefront (at the causal diagonal or the sequence end) run one at a time.
-  const int nun = min(nkt_u, nkt_w);
-  f32x16 s0, s1;
-  auto step = [&](auto r, auto next) __attribute__((always_inline)) {
-    f32x16& sc = decltype(r)::value ? s1 : s0;
-    f32x16& sn = decltype(r)::value ? s0 : s1;
-    sync();
-    f32x16 dp;
-    u32x4 b[2];
-    score(vptr(kt), doreg, dp);
-    softmax(kt, sc, std::false_type{});
-    if constexpr (decltype(next)::value) score(kptr(kt + 1), qreg, sn);
-    dscore(sc, dp, b);
-    accum(kt, b);
-    ++kt;
-  };
-  using T = std::true_type;
-  using F = std::false_type;
-  // Tile 0 is visible (first prologue barrier).
-  if (nun > 0) score(kptr(0), qreg, s0);
-  while (kt + 2 < nun) {
-    step(F{}, T{});
-    step(T{}, T{});
-  }
-  if (kt + 2 == nun) {
-    step(F{}, T{});
-    step(T{}, F{});
-  } else if (kt + 1 == nun) {
-    step(F{}, F{});
-  }
-  while (kt < nkt_w) {
-    sync();
-    f32x16 dp;
-    u32x4 b[2];
-    score(kptr(kt), qreg, s0);
-    score(vptr(kt), doreg, dp);
-    softmax(kt, s0, std::true_type{});
-    dscore(s0, dp, b);
-    accum(kt, b);
-    ++kt;
-  }
-  while (kt < nkt) {   // fully masked for this wavefront: loads only
-    sync();
-    ++kt;
-  }
+    f32x16 dqacc[D / 32];
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dqacc[db][r] = 0.f;
 
-  // Add the two partial accumulators of each row through LDS.  The pair
-  // splits the columns: the kb = 0 wavefront finalises d < D/2, the kb = 1
-  // one the rest.  Each hands its partial of the other half to its partner,
-  // adds the partner's partial to its own half, stages the bf16 half-rows in
-  // LDS and writes them out as whole half-rows (coalesced 16-byte stores).
-  __syncthreads();
-  u32x4* const red = reinterpret_cast<u32x4*>(smem);
-  constexpr int H = D / 64;   // 32-column blocks per half
-  constexpr int HS = H * 4;   // u32x4 slots per lane for one half
-  auto hand = [&](auto lo) __attribute__((always_inline)) {
+    // One tile, one 32-key half kb at a time (32 keys x 32 rows):
+    //   S^T = K Q^T and dP^T = V dO^T (MFMA);
+    //   P^T = exp2(s scale log2 e - L log2 e), masked only on tiles at the
+    //   causal diagonal or the sequence end, and dS^T = P^T (dP^T - Delta),
+    //   packed to bf16 (VALU);
+    //   dQ^T += K^T dS^T with K^T read transposed (MFMA).
+    auto compute = [&](int kt, auto masked) __attribute__((always_inline)) {
+      const uint32_t st = (uint32_t)(kt & 1) * SM::TILE;
+      const uint16_t* kc = reinterpret_cast<const uint16_t*>(smem + SM::K + st);
+      const uint16_t* vc = reinterpret_cast<const uint16_t*>(smem + SM::V + st);
 #pragma unroll
-    for (int i = 0; i < H; ++i)
+      for (int kb = 0; kb < 2; ++kb) {
+        const int ks0 = kt * kTileRows + 32 * kb;
+        // Under the causal mask a half whose first key follows the last row
+        // contributes nothing.
+        if constexpr (CAUSAL && decltype(masked)::value)
+          if (ks0 > qw0 + 31) continue;
+        f32x16 s, dp;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int db = decltype(lo)::value + i;
-        red[(wave * HS + 4 * i + j) * 64 + lane] =
-            u32x4{__float_as_uint(dqacc[db][4 * j]), __float_as_uint(dqacc[db][4 * j + 1]),
-                  __float_as_uint(dqacc[db][4 * j + 2]), __float_as_uint(dqacc[db][4 * j + 3])};
+        for (int r = 0; r < 16; ++r) {
+          s[r] = 0.f;
+          dp[r] = 0.f;
+        }
+#pragma unroll
+        for (int c = 0; c < D / 16; ++c) {
+          const int o = rr.rm[c] + 32 * kb * D;
+          s = mfma32(ld16(kc + o), qreg[c], s);
+          dp = mfma32(ld16(vc + o), doreg[c], dp);
+        }
+        // s[r]: key ks0 + 8(r/4) + 4half + r%4, query qrow.
+        const int t = ks0 + 4 * half - qrow;   // the lane's first key minus its query
+        const int u = ks0 + 4 * half - len;    // the lane's first key minus the end
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float pe = fast_exp2(__builtin_fmaf(s[r], sl2, -lse2));
+          if constexpr (decltype(masked)::value) {
+            const int off = 8 * (r / 4) + (r % 4);
+            if constexpr (CAUSAL) pe = t + off > 0 ? 0.f : pe;   // key after query
+            pe = u + off >= 0 ? 0.f : pe;                        // key past the end
+          }
+          s[r] = pe * (dp[r] - delta);
+        }
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const u32x4 b = pack_chunk(s, c);
+          const int rc = 16 * (2 * kb + c) * D;
+#pragma unroll
+          for (int db = 0; db < D / 32; ++db) {
+            const u32x2 lo = ld_tr(kc + trr.tr[db][0] + rc), hi = ld_tr(kc + trr.tr[db][1] + rc);
+            dqacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, b, dqacc[db]);
+          }
+        }
       }
-  };
-  if (kb == 0)
-    hand(std::integral_constant<int, H>{});
-  else
-    hand(std::integral_constant<int, 0>{});
-  __syncthreads();
-  auto finalize = [&](auto lo) __attribute__((always_inline)) {
-    constexpr int db0 = decltype(lo)::value;
-    const u32x4* src = red + (wave ^ 4) * HS * 64;
+    };
+
+    // Tile kt: wait for this wavefront's copies of it, then the barrier makes
+    // every wavefront's share visible and frees the other stage (tile kt - 1),
+    // which tile kt + 1 now fills (tile 1 went out with tile 0).
+    int kt = 0;
+    auto sync = [&]() __attribute__((always_inline)) {
+      if (kt == 0 && nkt > 1)
+        wait_vm_upto<2 * Tile::NJ>();
+      else
+        wait_vm_all();
+      __syncthreads();
+      if (kt > 0 && kt + 1 < nkt) issue(kt + 1);
+    };
+    // Key tiles past this wavefront's last row are fully masked for it.
+    const int nkt_w = qw0 >= len ? 0 : CAUSAL ? min(nkt, (qw0 + 31) / kTileRows + 1) : nkt;
+    // Tiles [0, nkt_u) need no mask for any of the wavefront's rows.
+    const int nkt_u = min(nkt_w, CAUSAL ? min((qw0 + 1) / kTileRows, len / kTileRows)
+                                        : len / kTileRows);
+    while (kt < nkt_u) {
+      sync();
+      compute(kt, std::false_type{});
+      ++kt;
+    }
+    while (kt < nkt_w) {
+      sync();
+      compute(kt, std::true_type{});
+      ++kt;
+    }
+    while (kt < nkt) {   // fully masked for this wavefront: loads only
+      sync();
+      ++kt;
+    }
+
+    // Epilogue: scaled dQ rows staged as bf16 in LDS (this wavefront's own
+    // region, 16-byte chunks swizzled by row), then written out as whole
+    // rows (coalesced 16-byte stores).
+    __syncthreads();   // every wavefront is done with the stages
+    uint16_t* stg = reinterpret_cast<uint16_t*>(smem + wave * 32 * D * 2);
+    const int sw = tile_swz<D>(l32);
 #pragma unroll
-    for (int i = 0; i < H; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const u32x4 pp = src[(4 * i + j) * 64 + lane];
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          dqacc[db0 + i][4 * j + e] = (dqacc[db0 + i][4 * j + e] + __uint_as_float(pp[e])) * a.scale;
-      }
-    // Stage [32 rows][D/2] bf16 in the partner's region (read above); the
-    // 16-byte chunks of a half-row are swizzled by the row's low bits.
-    constexpr int CPR = D / 16;   // chunks per half-row
-    uint16_t* stg = reinterpret_cast<uint16_t*>(red + (wave ^ 4) * HS * 64);
-    const int sw = l32 & (CPR - 1);
-#pragma unroll
-    for (int i = 0; i < H; ++i)
+    for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const f32x16& v = dqacc[db0 + i];
-        st8(stg + l32 * (D / 2) + 8 * ((4 * i + g) ^ sw) + 4 * half,
-            u32x2{pack_bf16(v[4 * g], v[4 * g + 1]), pack_bf16(v[4 * g + 2], v[4 * g + 3])});
+        const f32x16& v = dqacc[db];
+        st8(stg + l32 * D + 8 * ((4 * db + g) ^ sw) + 4 * half,
+            u32x2{pack_bf16(v[4 * g] * scale, v[4 * g + 1] * scale),
+                  pack_bf16(v[4 * g + 2] * scale, v[4 * g + 3] * scale)});
       }
-    uint16_t* const dqp = a.dq + qoff + 32 * db0;
+    constexpr int CPR = D / 8;
+    uint16_t* const dqp = a.dq + qoff;
 #pragma unroll
     for (int i = 0; i < 32 * CPR / 64; ++i) {
       const int pidx = i * 64 + lane;
       const int row = pidx / CPR, ch = pidx % CPR;
-      const u32x4 v = ld16(stg + row * (D / 2) + 8 * (ch ^ (row & (CPR - 1))));
-      if (qw0 + row < len) st16(dqp + (int64_t)(qw0 + row) * L.q_row + 8 * ch, v);
+      const u32x4 v = ld16(stg + row * D + 8 * (ch ^ tile_swz<D>(row)));
+      if (qw0 + row < len) st16(dqp + (int64_t)(qw0 + row) * q_row + 8 * ch, v);
     }
-  };
-  if (kb == 0)
-    finalize(std::integral_constant<int, 0>{});
-  else
-    finalize(std::integral_constant<int, H>{});
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -630,7 +541,8 @@ template __global__ void bwd_dkdv_kernel<128, true>(BwdArgs);
 }  // namespace
 
 hipError_t launch_bwd(const BwdArgs& a, int D, int phases, hipStream_t stream) {
-  const dim3 gq((unsigned)(a.L.nseg * a.L.Hq), (unsigned)((a.L.S + kQM - 1) / kQM));
+  // A dQ workgroup takes a query block and its mirror (see the kernel).
+  const dim3 gq((unsigned)(a.L.nseg * a.L.Hq), (unsigned)(((a.L.S + kQM - 1) / kQM + 1) / 2));
   const dim3 gk((unsigned)(a.L.nseg * a.L.Hkv), (unsigned)((a.L.S + kKN - 1) / kKN));
   if (phases & 1) {
     if (D == 64) {

@@ -59,21 +59,8 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 __device__ __forceinline__ float swap_halves(float x) { return __shfl_xor(x, 32); }
 
 __device__ __forceinline__ u32x4 ld16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
-__device__ __forceinline__ u32x2 ld8(const uint16_t* p) { return *reinterpret_cast<const u32x2*>(p); }
 __device__ __forceinline__ void st16(uint16_t* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
 __device__ __forceinline__ void st8(uint16_t* p, u32x2 v) { *reinterpret_cast<u32x2*>(p) = v; }
-
-// 4 rows x 8 bf16 (one u32x4 per row) -> 8 columns x 4 bf16 (one u32x2 per
-// column): out[c] = {row0[c], row1[c], row2[c], row3[c]}.
-__device__ __forceinline__ void transpose4x8(const u32x4 (&in)[4], u32x2 (&out)[8]) {
-#pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    out[2 * m][0] = (in[0][m] & 0xffffu) | (in[1][m] << 16);
-    out[2 * m][1] = (in[2][m] & 0xffffu) | (in[3][m] << 16);
-    out[2 * m + 1][0] = (in[0][m] >> 16) | (in[1][m] & 0xffff0000u);
-    out[2 * m + 1][1] = (in[2][m] >> 16) | (in[3][m] & 0xffff0000u);
-  }
-}
 
 // Wavefront index as a scalar (the compiler cannot prove threadIdx.x >> 6 is
 // uniform, and a uniform value keeps wave-level decisions as scalar branches).
@@ -104,61 +91,11 @@ __device__ __forceinline__ rsrc_t rows_rsrc(const uint16_t* head_base, int row0,
 }
 
 // ---------------------------------------------------------------------------
-// LDS tile layouts.  gfx950's LDS serves 64 banks x 4 bytes per cycle (a
-// 16-byte access 16 lanes at a time, an 8-byte access 32 lanes at a time);
-// the layouts below are also conflict-free under a 32-bank model.
-//
-// Row-major tile [64][D] filled by 4-row x 8-column blocks, rows unpadded:
-// the 16-byte chunk c of row r lives at chunk c ^ swz_row<D>(r).  The
-// swizzle is a GF(2)-linear map of the row bits chosen so that sixteen
-// consecutive rows at one chunk (MFMA operand reads) and the block stores of
-// sixteen lanes (8 row groups x 2 chunks) hit distinct banks; for D = 64 the
-// two chunks of a store phase also take rows of opposite parity (see
-// store_row_order).
-template <int D>
-__device__ __forceinline__ int swz_row(int r) {
-  if constexpr (D == 128)
-    return (r & 7) ^ (((r >> 3) & 1) * 9) ^ (((r >> 4) & 1) * 2);
-  else
-    return (r & 7) ^ ((r >> 3) & 3);
-}
-
-// Row (0..3) of its 4-row block that a thread stores at step i.
-template <int D>
-__device__ __forceinline__ int store_row_order(int i, int cc) {
-  if constexpr (D == 64)
-    return i ^ (cc & 1);
-  else
-    return i;
-}
-
-// Transposed tile [D][64] with rows padded to 68 bf16 (136 bytes): sixteen
-// consecutive rows at one column, and one row at sixteen 8-byte chunks, both
-// land on sixteen distinct bank pairs.
-constexpr int kTS = 68;
-
-// Thread -> 4x8 block assignment for a tile of 64 rows x D columns
-// (16 row groups x D/8 column chunks): within every 16 lanes, 8 row groups
-// x 2 column chunks, so that the transposed 8-byte stores of 16 lanes and
-// the row-major 16-byte stores of 8 lanes are free of bank conflicts, and a
-// global load instruction reads 128 contiguous bytes from each of 8 rows.
-template <int D>
-struct BlockMap {
-  static constexpr int CPR = D / 8;            // column chunks
-  static constexpr int NBLK = 16 * CPR;        // blocks per 64-row tile
-  int rg, cc;                                  // row group (rows 4rg..4rg+3), column chunk
-  bool active;
-  __device__ __forceinline__ explicit BlockMap(int tid) {
-    active = tid < NBLK;
-    rg = (tid & 7) + 8 * (tid / (8 * CPR));
-    cc = (tid >> 3) % CPR;
-  }
-};
-
-// ---------------------------------------------------------------------------
 // Asynchronous tiles: [64 rows][D] bf16 tiles filled straight from global
 // memory into LDS (buffer_load ... lds) and read back either row-major
-// (16-byte MFMA operand rows) or transposed (ds_read_b64_tr_b16).
+// (16-byte MFMA operand rows) or transposed (ds_read_b64_tr_b16).  gfx950's
+// LDS serves 64 banks x 4 bytes: a 16-byte access 16 lanes at a time, an
+// 8-byte access 32 lanes at a time.
 //
 // A DMA load writes 16 bytes per lane to consecutive LDS addresses (lane L
 // of the wave at base + 16 L), so the layout is chosen by which source chunk
@@ -319,11 +256,6 @@ __device__ __forceinline__ void wait_vm_upto() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
-
-// Scheduling-group masks for __builtin_amdgcn_sched_group_barrier.
-constexpr int kSgMfma = 0x008;
-constexpr int kSgValu = 0x002;
-constexpr int kSgDsRead = 0x100;
 
 // Resolve segment z of a layout: first row offset (elements) and length.
 // Packed offsets are clamped into [0, total] so a malformed cu_seqlens array

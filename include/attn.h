@@ -79,14 +79,15 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
              int B, int Hq, int Hkv, int S, int D, int causal, float scale,
              hipStream_t stream);
 
-/* Bytes of backward workspace for the fixed-length layout (fp32 Delta). */
+/* Bytes of backward workspace for the fixed-length layout (fp32 Delta and
+ * fp32 L log2(e), one of each per query row and head). */
 size_t attn_bwd_workspace_size(int B, int Hq, int Hkv, int S, int D);
 
 /*
  * Backward, fixed length.  Consumes q, k, v, the forward's o and lse, and
  * dO; writes dq [B,Hq,S,D] and dk, dv [B,Hkv,S,D] (dk, dv summed over each
- * query-head group).  Delta_i = sum_d dO_id * O_id is precomputed into the
- * workspace; P is recomputed from lse.  The gradients are of the loss
+ * query-head group).  Delta_i = sum_d dO_id * O_id and lse_i * log2(e) are
+ * precomputed into the workspace; P is recomputed from them.  The gradients are of the loss
  * sum(dO * O) with O = attention(q, k, v).  The result is deterministic
  * (no atomics).
  */
@@ -105,7 +106,8 @@ int attn_fwd_varlen(const void* q, const void* k, const void* v, void* o,
                     int max_seqlen, int total, int Hq, int Hkv, int D,
                     int causal, float scale, hipStream_t stream);
 
-/* Bytes of backward workspace for the packed layout (fp32 Delta). */
+/* Bytes of backward workspace for the packed layout (fp32 Delta and fp32
+ * L log2(e), one of each per query row and head). */
 size_t attn_bwd_varlen_workspace_size(int total, int Hq, int Hkv, int D);
 
 /* Backward, packed variable length.  Same contract as attn_bwd. */
@@ -119,8 +121,9 @@ int attn_bwd_varlen(const void* q, const void* k, const void* v,
 /*
  * The backward in separately enqueued phases, for callers that time or
  * schedule its two kernels on their own.  `phases` is a bit mask:
- *   ATTN_BWD_DQ   computes Delta into the workspace, then dq;
- *   ATTN_BWD_DKDV computes dk and dv from the Delta of an ATTN_BWD_DQ phase
+ *   ATTN_BWD_DQ   computes Delta and lse * log2(e) into the workspace,
+ *                 then dq;
+ *   ATTN_BWD_DKDV computes dk and dv from the workspace of an ATTN_BWD_DQ phase
  *                 enqueued earlier on the same stream with the same
  *                 workspace and inputs.
  * phases = ATTN_BWD_DQ | ATTN_BWD_DKDV is exactly attn_bwd / attn_bwd_varlen;

@@ -125,6 +125,7 @@ int bwd_common(const void* q, const void* k, const void* v, const void* o, const
   a.dk = static_cast<uint16_t*>(dk);
   a.dv = static_cast<uint16_t*>(dv);
   a.delta = static_cast<float*>(ws);
+  a.lse2 = reinterpret_cast<float*>(static_cast<char*>(ws) + ws_need / 2);
   a.scale = scale;
   a.scale_log2 = scale * 1.4426950408889634f;
   a.causal = causal;
@@ -132,8 +133,9 @@ int bwd_common(const void* q, const void* k, const void* v, const void* o, const
 }
 
 size_t delta_bytes(int64_t rows_times_heads) {
-  // fp32 Delta per (row, query head), rounded up to 256 bytes.
-  return (size_t)((rows_times_heads * 4 + 255) / 256 * 256);
+  // fp32 Delta and fp32 L log2(e) per (row, query head), each array rounded
+  // up to 256 bytes.
+  return 2 * (size_t)((rows_times_heads * 4 + 255) / 256 * 256);
 }
 
 }  // namespace

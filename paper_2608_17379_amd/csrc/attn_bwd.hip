@@ -11,9 +11,9 @@
 //  * bwd_dq_kernel: one workgroup of 4 wavefronts per (segment, query head,
 //    128-row query block and its causal mirror), 32 rows per wavefront, two
 //    workgroups per CU.  Its prologue computes Delta for its rows (the rows'
-//    dO and O are read once) and stores it in the workspace; the loop over
-//    key tiles recomputes S^T = K Q^T and dP^T = V dO^T, forms dS^T in
-//    registers and accumulates dQ^T += K^T dS^T.
+//    dO and O are read once) and stores it, with L log2(e), in the
+//    workspace; the loop over key tiles recomputes S^T = K Q^T and
+//    dP^T = V dO^T, forms dS^T in registers and accumulates dQ^T += K^T dS^T.
 //  * bwd_dkdv_kernel: one workgroup of 8 wavefronts per (segment, key/value
 //    head, 128 keys), launched after bwd_dq_kernel (it reads Delta).  The
 //    workgroup keeps its K and V rows in LDS and loops over every query head
@@ -153,7 +153,10 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
           dsum += bf16_lo(doreg[c][w]) * bf16_lo(ov[c][w]) + bf16_hi(doreg[c][w]) * bf16_hi(ov[c][w]);
     }
     const float delta = dsum + swap_halves(dsum);
-    if (valid && half == 0) a.delta[roff + qrow] = delta;
+    if (valid && half == 0) {
+      a.delta[roff + qrow] = delta;
+      a.lse2[roff + qrow] = lse2;
+    }
 
     f32x16 dqacc[D / 32];
 #pragma unroll
@@ -335,7 +338,7 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
   // kernel argument itself would make the compiler spill it to scratch).
   const uint16_t* const qbase = a.q;
   const uint16_t* const dobase = a.dout;
-  const float* const lsebase = a.lse;
+  const float* const lsebase = a.lse2;   // lse * log2(e), written by the dQ kernel
   const float* const delbase = a.delta;
   const int group = L.group;
   const int64_t q_head = L.q_head, r_head = L.r_head;
@@ -425,7 +428,7 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = 4 * g + i;
-        float p = fast_exp2(__builtin_fmaf(s[r], sl2, -l4[i] * kLog2e));
+        float p = fast_exp2(__builtin_fmaf(s[r], sl2, -l4[i]));
         if constexpr (decltype(masked)::value) p = t > 8 * g + i ? 0.f : p;   // key after query
         s[r] = p;
         dp[r] = p * (dp[r] - d4[i]);

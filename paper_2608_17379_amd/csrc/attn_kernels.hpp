@@ -49,7 +49,8 @@ struct BwdArgs {
   uint16_t* dq;
   uint16_t* dk;
   uint16_t* dv;
-  float* delta;            // workspace, same layout as lse
+  float* delta;            // workspace: Delta, same layout as lse
+  float* lse2;             // workspace: lse * log2(e), same layout as lse
   float scale;             // softmax scale
   float scale_log2;        // scale * log2(e)
   int causal;

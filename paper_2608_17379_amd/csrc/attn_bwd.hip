@@ -281,17 +281,20 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
 // ---------------------------------------------------------------------------
 // dK, dV
 //
-// Eight wavefronts per workgroup of 128 keys: wavefronts w and w + 4 (which
-// share a SIMD) own the same 32 keys and take the two 32-query halves of
-// every 64-query tile, so each SIMD runs two independent wavefronts whose
-// MFMA, VALU and LDS work interleave in hardware.  K and V of the
-// workgroup's keys stay in LDS (read as B operands), the query-side tiles
-// (Q, dO, L, Delta) stream through two LDS stages, and the two partial dK/dV
-// accumulators of each key are added through LDS at the end.
+// A workgroup covers 128 keys, 32 per wavefront group.  K and V of the
+// workgroup's keys stay in LDS (read as B operands) and the query-side tiles
+// (Q, dO, L log2 e, Delta) stream through two LDS stages.
+//  * D = 128: eight wavefronts; wavefronts w and w + 4 (which share a SIMD)
+//    own the same 32 keys and take the two 32-query halves of every 64-query
+//    tile, and their two partial dK/dV accumulators are added through LDS at
+//    the end (one workgroup per CU: 129 KiB of LDS).
+//  * D = 64: four wavefronts, each taking both halves of every tile, and two
+//    workgroups per CU (65 KiB of LDS each), so that the two wavefronts on a
+//    SIMD belong to different workgroups and are not held in step.
 // ---------------------------------------------------------------------------
 constexpr int kKN = 128;        // keys per workgroup
-constexpr int kDkvWaves = 8;
-constexpr int kDkvThreads = 64 * kDkvWaves;
+template <int D>
+constexpr int dkv_waves() { return D == 64 ? 4 : 8; }
 
 template <int D>
 struct DkvSmem {
@@ -303,13 +306,17 @@ struct DkvSmem {
   static constexpr int LSE = DO + 2 * TILE;                // 2 stages x 64 fp32
   static constexpr int DEL = LSE + 2 * 256;
   static constexpr int BYTES = DEL + 2 * 256;
-  // epilogue: one tensor's partial per wavefront, (D/32) x 4 u32x4 per lane
-  static_assert(8 * (D / 32) * 4 * 1024 <= BYTES, "reduction buffer");
+  // epilogue: one tensor's fp32 partial per wavefront (pairs), or the bf16
+  // dK and dV rows of each wavefront
+  static_assert(dkv_waves<D>() * (D / 32) * 4 * 1024 <= BYTES, "reduction buffer");
+  static_assert(dkv_waves<D>() * 2 * 32 * D * 2 <= BYTES, "epilogue staging");
 };
 
 template <int D, bool CAUSAL>
-__global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
-  using Tile = AsyncTile<D, kDkvWaves>;
+__global__ __launch_bounds__(64 * dkv_waves<D>(), D == 64 ? 2 : 1) void bwd_dkdv_kernel(BwdArgs a) {
+  constexpr int NW = dkv_waves<D>();
+  constexpr bool PAIRS = NW == 8;   // two wavefronts per key group
+  using Tile = AsyncTile<D, NW>;
   using SM = DkvSmem<D>;
   __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
   uint16_t* const sk = reinterpret_cast<uint16_t*>(smem + SM::K);
@@ -318,8 +325,8 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = wave_id();
   const int l32 = lane & 31, half = lane >> 5;
-  const int kq = wave & 3;    // 32-key group
-  const int sb = wave >> 2;   // which 32-query half of each tile
+  const int kq = wave & 3;            // 32-key group
+  const int sb = PAIRS ? wave >> 2 : 0;   // query half of each tile (pairs only)
 
   const Layout L = a.L;
   const int z = blockIdx.x / L.Hkv, hk = blockIdx.x % L.Hkv;
@@ -400,12 +407,14 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
   const uint16_t* const krd = sk + (kq >> 1) * (SM::TILE / 2) + 32 * (kq & 1) * D;
   const uint16_t* const vrd = sv + (kq >> 1) * (SM::TILE / 2) + 32 * (kq & 1) * D;
 
-  auto compute = [&](int n, int st, auto masked) __attribute__((always_inline)) {
+  // Query half hq (32 queries) of tile n, in stage st, against this
+  // wavefront's 32 keys.
+  auto compute = [&](int n, int st, int hq, auto masked) __attribute__((always_inline)) {
     const uint16_t* q = reinterpret_cast<const uint16_t*>(smem + SM::Q + st * SM::TILE);
     const uint16_t* dout = reinterpret_cast<const uint16_t*>(smem + SM::DO + st * SM::TILE);
     const float* lse = reinterpret_cast<const float*>(smem + SM::LSE + st * 256);
     const float* del = reinterpret_cast<const float*>(smem + SM::DEL + st * 256);
-    const int qs0 = (it0 + n % per_head) * kTileRows + 32 * sb;
+    const int qs0 = (it0 + n % per_head) * kTileRows + 32 * hq;
     // S = Q K^T, dP = dO V^T for this wavefront's 32 queries x 32 keys.
     f32x16 s, dp;
 #pragma unroll
@@ -415,7 +424,7 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
     }
 #pragma unroll
     for (int c = 0; c < D / 16; ++c) {
-      const int o = rr.rm[c] + 32 * sb * D;
+      const int o = rr.rm[c] + 32 * hq * D;
       s = mfma32(ld16(q + o), ld16(krd + rr.rm[c]), s);
       dp = mfma32(ld16(dout + o), ld16(vrd + rr.rm[c]), dp);
     }
@@ -423,8 +432,8 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
     const int t = krow - qs0 - 4 * half;   // key minus the lane's first query
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse[32 * sb + 8 * g + 4 * half]);
-      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&del[32 * sb + 8 * g + 4 * half]);
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse[32 * hq + 8 * g + 4 * half]);
+      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&del[32 * hq + 8 * g + 4 * half]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = 4 * g + i;
@@ -440,7 +449,7 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
     for (int c = 0; c < 2; ++c) {
       const u32x4 pb = pack_chunk(s, c);
       const u32x4 dsb = pack_chunk(dp, c);
-      const int rc = 16 * (2 * sb + c) * D;
+      const int rc = 16 * (2 * hq + c) * D;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
         const u32x2 dlo = ld_tr(dout + trr.tr[db][0] + rc), dhi = ld_tr(dout + trr.tr[db][1] + rc);
@@ -461,7 +470,12 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
     wait_vm_all();
     __syncthreads();
     if (n + 1 < niter) issue(n + 1, (n + 1) & 1);
-    compute(n, n & 1, masked);
+    if constexpr (PAIRS) {
+      compute(n, n & 1, sb, masked);
+    } else {
+      compute(n, n & 1, 0, masked);
+      compute(n, n & 1, 1, masked);
+    }
   };
   const int nmask = CAUSAL ? min(2, per_head) : 0;
   issue(0, 0);
@@ -472,49 +486,21 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
     for (; n < nend; ++n) step(n, std::false_type{});
   }
 
-  // Add the two partial accumulators of each key through LDS.  The pair
-  // splits the work: the sb = 0 wavefront finalises dK, the sb = 1 one dV.
-  // Each first hands its partial of the other tensor to its partner, then
-  // adds the partner's partial to its own, stages the bf16 rows in LDS and
-  // writes them out as whole rows (coalesced 16-byte stores).
-  __syncthreads();
-  u32x4* const red = reinterpret_cast<u32x4*>(smem);
-  constexpr int SL = (D / 32) * 4;   // u32x4 slots per lane for one tensor
-  auto hand = [&](const f32x16 (&acc)[D / 32]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        red[(wave * SL + 4 * db + j) * 64 + lane] =
-            u32x4{__float_as_uint(acc[db][4 * j]), __float_as_uint(acc[db][4 * j + 1]),
-                  __float_as_uint(acc[db][4 * j + 2]), __float_as_uint(acc[db][4 * j + 3])};
-  };
-  if (sb == 0)
-    hand(dvacc);
-  else
-    hand(dkacc);
-  __syncthreads();
+  // Epilogue.  Rows are staged as bf16 in LDS ([32 keys][D], 16-byte chunks
+  // swizzled by row as in the tiles) and written out as whole rows
+  // (coalesced 16-byte stores).
+  __syncthreads();   // every wavefront is done with the tiles
   const int64_t kv_row = L.kv_row;
-  auto finalize = [&](f32x16 (&acc)[D / 32], float mul, uint16_t* gout) __attribute__((always_inline)) {
-    const u32x4* src = red + (wave ^ 4) * SL * 64;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const u32x4 pp = src[(4 * db + j) * 64 + lane];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc[db][4 * j + i] = (acc[db][4 * j + i] + __uint_as_float(pp[i])) * mul;
-      }
-    // Stage [32 keys][D] bf16 in the partner's region (read above), 16-byte
-    // chunks swizzled by row as in the tiles.
-    uint16_t* stg = reinterpret_cast<uint16_t*>(red + (wave ^ 4) * SL * 64);
+  auto store_rows = [&](const f32x16 (&acc)[D / 32], float mul, uint16_t* stg, uint16_t* gout)
+      __attribute__((always_inline)) {
     const int sw = tile_swz<D>(l32);
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int g = 0; g < 4; ++g)
         st8(stg + l32 * D + 8 * ((4 * db + g) ^ sw) + 4 * half,
-            u32x2{pack_bf16(acc[db][4 * g], acc[db][4 * g + 1]), pack_bf16(acc[db][4 * g + 2], acc[db][4 * g + 3])});
+            u32x2{pack_bf16(acc[db][4 * g] * mul, acc[db][4 * g + 1] * mul),
+                  pack_bf16(acc[db][4 * g + 2] * mul, acc[db][4 * g + 3] * mul)});
     constexpr int CPR = D / 8;
 #pragma unroll
     for (int i = 0; i < 32 * CPR / 64; ++i) {
@@ -524,10 +510,49 @@ __global__ __launch_bounds__(kDkvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
       if (kw0 + row < len) st16(gout + (int64_t)(kw0 + row) * kv_row + 8 * ch, v);
     }
   };
-  if (sb == 0)
-    finalize(dkacc, a.scale, a.dk + kvoff);
-  else
-    finalize(dvacc, 1.f, a.dv + kvoff);
+  if constexpr (!PAIRS) {
+    // Each wavefront holds the whole of its keys' dK and dV.
+    uint16_t* stg = reinterpret_cast<uint16_t*>(smem) + wave * 2 * 32 * D;
+    store_rows(dkacc, a.scale, stg, a.dk + kvoff);
+    store_rows(dvacc, 1.f, stg + 32 * D, a.dv + kvoff);
+  } else {
+    // The pair splits the work: the sb = 0 wavefront finalises dK, the
+    // sb = 1 one dV.  Each first hands its partial of the other tensor to
+    // its partner, then adds the partner's partial to its own.
+    u32x4* const red = reinterpret_cast<u32x4*>(smem);
+    constexpr int SL = (D / 32) * 4;   // u32x4 slots per lane for one tensor
+    auto hand = [&](const f32x16 (&acc)[D / 32]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          red[(wave * SL + 4 * db + j) * 64 + lane] =
+              u32x4{__float_as_uint(acc[db][4 * j]), __float_as_uint(acc[db][4 * j + 1]),
+                    __float_as_uint(acc[db][4 * j + 2]), __float_as_uint(acc[db][4 * j + 3])};
+    };
+    if (sb == 0)
+      hand(dvacc);
+    else
+      hand(dkacc);
+    __syncthreads();
+    auto finalize = [&](f32x16 (&acc)[D / 32], float mul, uint16_t* gout) __attribute__((always_inline)) {
+      const u32x4* src = red + (wave ^ 4) * SL * 64;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const u32x4 pp = src[(4 * db + j) * 64 + lane];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[db][4 * j + i] += __uint_as_float(pp[i]);
+        }
+      // Staged in the partner's region, read above.
+      store_rows(acc, mul, reinterpret_cast<uint16_t*>(red + (wave ^ 4) * SL * 64), gout);
+    };
+    if (sb == 0)
+      finalize(dkacc, a.scale, a.dk + kvoff);
+    else
+      finalize(dvacc, 1.f, a.dv + kvoff);
+  }
 }
 
 // Explicit instantiations: without them the host compiler may skip the
@@ -563,14 +588,14 @@ hipError_t launch_bwd(const BwdArgs& a, int D, int phases, hipStream_t stream) {
   if (phases & 2) {
     if (D == 64) {
       if (a.causal)
-        hipLaunchKernelGGL((bwd_dkdv_kernel<64, true>), gk, dim3(kDkvThreads), 0, stream, a);
+        hipLaunchKernelGGL((bwd_dkdv_kernel<64, true>), gk, dim3(64 * dkv_waves<64>()), 0, stream, a);
       else
-        hipLaunchKernelGGL((bwd_dkdv_kernel<64, false>), gk, dim3(kDkvThreads), 0, stream, a);
+        hipLaunchKernelGGL((bwd_dkdv_kernel<64, false>), gk, dim3(64 * dkv_waves<64>()), 0, stream, a);
     } else {
       if (a.causal)
-        hipLaunchKernelGGL((bwd_dkdv_kernel<128, true>), gk, dim3(kDkvThreads), 0, stream, a);
+        hipLaunchKernelGGL((bwd_dkdv_kernel<128, true>), gk, dim3(64 * dkv_waves<128>()), 0, stream, a);
       else
-        hipLaunchKernelGGL((bwd_dkdv_kernel<128, false>), gk, dim3(kDkvThreads), 0, stream, a);
+        hipLaunchKernelGGL((bwd_dkdv_kernel<128, false>), gk, dim3(64 * dkv_waves<128>()), 0, stream, a);
     }
   }
   return hipGetLastError();

@@ -14,20 +14,21 @@
 //    dO and O are read once) and stores it, with L log2(e), in the
 //    workspace; the loop over key tiles recomputes S^T = K Q^T and
 //    dP^T = V dO^T, forms dS^T in registers and accumulates dQ^T += K^T dS^T.
-//  * bwd_dkdv_kernel: one workgroup of 8 wavefronts per (segment, key/value
-//    head, 128 keys), launched after bwd_dq_kernel (it reads Delta).  The
-//    workgroup keeps its K and V rows in LDS and loops over every query head
-//    of the group and every query tile that can see its keys, accumulating
-//    dV^T += dO^T P and dK^T += Q^T dS in registers; the grouped-query sum
-//    therefore needs no cross-workgroup reduction.
+//  * bwd_dkdv_kernel: one workgroup per (segment, key/value head, 128 keys)
+//    (8 wavefronts at D = 128, 4 at D = 64), launched after bwd_dq_kernel
+//    (it reads the workspace).  The workgroup keeps its K and V rows in LDS
+//    and loops over every query head of the group and every query tile that
+//    can see its keys, accumulating dV^T += dO^T P and dK^T += Q^T dS in
+//    registers; the grouped-query sum therefore needs no cross-workgroup
+//    reduction.
 //
-// Tiles of 64 rows (K and V for dQ; Q, dO, L and Delta for dK/dV) go from
-// global memory straight into a ring of LDS stages (buffer_load ... lds,
+// Tiles of 64 rows (K and V for dQ; Q, dO, L log2 e and Delta for dK/dV) go
+// from global memory straight into a ring of LDS stages (buffer_load ... lds,
 // bounded at the segment end so that rows past it read as zero), issued a
-// tile ahead with one barrier per tile.  They stay row-major in LDS: operands whose
-// reduction index runs along the tile's rows (K^T, Q^T, dO^T) come out of the
-// same tiles through the transposing read ds_read_b64_tr_b16.  Accumulator
-// tiles are fed back as B operands directly (device_common.hpp).
+// tile ahead with one barrier per tile.  They stay row-major in LDS: operands
+// whose reduction index runs along the tile's rows (K^T, Q^T, dO^T) come out
+// of the same tiles through the transposing read ds_read_b64_tr_b16.
+// Accumulator tiles are fed back as B operands directly (device_common.hpp).
 //
 // The backward expects a finite L for every row that has a visible key (as
 // the forward produces); rows past the segment end read L = Delta = 0 and

@@ -24,7 +24,7 @@ Per-launch algorithmic FLOP of each kernel:
 with F the forward FLOP above.  `traffic` (HBM bytes per launch from
 rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a copy-kernel calibration) is
 read from profiles/traffic.json when that file was taken on the current
-kernel source, else null.
+kernel source (comments aside), else null.
 
 The CPU baseline times the fp64 oracle (test infrastructure, used here only
 for this leg) on a bounded sample of the same workload: whole (batch, head)
@@ -62,8 +62,15 @@ def fwd_flops(w, cu_seqlens=None) -> float:
 
 
 def source_sha(kernel: str) -> str:
+    """Hash of the kernel's source with comments and blank lines removed, so
+    that a recorded traffic figure survives comment-only edits."""
     path = os.path.join(ROOT, "paper_2608_17379_amd", "csrc", KERNEL_SOURCES[kernel])
-    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+    code = []
+    for line in open(path, encoding="utf-8"):
+        line = line.split("//", 1)[0].rstrip()
+        if line:
+            code.append(line)
+    return hashlib.sha256("\n".join(code).encode()).hexdigest()[:16]
 
 
 def load_traffic(kernel: str, workload: str):

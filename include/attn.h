@@ -62,7 +62,7 @@ typedef enum {
   ATTN_ERR_SHAPE = -2,      /* a size is negative, Hq/Hkv < 1, or too large
                                (S or max_seqlen > 65535*128, Hq*D > 2^22) */
   ATTN_ERR_GQA = -3,        /* Hq is not a multiple of Hkv */
-  ATTN_ERR_HEAD_DIM = -4,   /* D is not 64 or 128 */
+  ATTN_ERR_HEAD_DIM = -4,   /* D is not 64, 96 or 128 */
   ATTN_ERR_ALIGN = -5,      /* a pointer is not 16-byte aligned */
   ATTN_ERR_WORKSPACE = -6,  /* workspace null or smaller than required */
   ATTN_ERR_HIP = -7,        /* a kernel launch failed (hipGetLastError) */

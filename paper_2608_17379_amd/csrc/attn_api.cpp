@@ -20,7 +20,7 @@ bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) !
 int check_common(int Hq, int Hkv, int D, int causal, float scale) {
   if (Hq < 1 || Hkv < 1) return ATTN_ERR_SHAPE;
   if (Hq % Hkv != 0) return ATTN_ERR_GQA;
-  if (D != 64 && D != 128) return ATTN_ERR_HEAD_DIM;
+  if (D != 64 && D != 96 && D != 128) return ATTN_ERR_HEAD_DIM;
   // Bytes of 128 rows of one packed tensor must fit the 31-bit offsets of
   // the kernels' buffer loads.
   if ((int64_t)Hq * D * 2 * 128 > 0x7fffffff) return ATTN_ERR_SHAPE;
@@ -239,7 +239,7 @@ const char* attn_status_string(int status) {
     case ATTN_ERR_NULL: return "a required pointer is null";
     case ATTN_ERR_SHAPE: return "a size is negative, a head count is below 1, or a size is too large";
     case ATTN_ERR_GQA: return "Hq is not a multiple of Hkv";
-    case ATTN_ERR_HEAD_DIM: return "head dimension must be 64 or 128";
+    case ATTN_ERR_HEAD_DIM: return "head dimension must be 64, 96 or 128";
     case ATTN_ERR_ALIGN: return "a pointer is not 16-byte aligned";
     case ATTN_ERR_WORKSPACE: return "workspace is null or smaller than attn_bwd_workspace_size()";
     case ATTN_ERR_HIP: return "a kernel launch failed";

@@ -15,7 +15,7 @@
 //    workspace; the loop over key tiles recomputes S^T = K Q^T and
 //    dP^T = V dO^T, forms dS^T in registers and accumulates dQ^T += K^T dS^T.
 //  * bwd_dkdv_kernel: one workgroup per (segment, key/value head, 128 keys)
-//    (8 wavefronts at D = 128, 4 at D = 64), launched after bwd_dq_kernel
+//    (8 wavefronts at D = 128 and 96, 4 at D = 64), launched after bwd_dq_kernel
 //    (it reads the workspace).  The workgroup keeps its K and V rows in LDS
 //    and loops over every query head of the group and every query tile that
 //    can see its keys, accumulating dV^T += dO^T P and dK^T += Q^T dS in
@@ -61,17 +61,19 @@ constexpr int kDqThreads = 64 * kDqWaves;
 
 template <int D>
 struct DqSmem {
-  static constexpr int TILE = 64 * D * 2;   // bytes of a 64-row bf16 tile
+  static constexpr int P = lds_pitch<D>();  // LDS row pitch (elements)
+  static constexpr int TILE = 64 * P * 2;   // bytes of a 64-row bf16 tile
   static constexpr int K = 0;               // 2 stages
   static constexpr int V = K + 2 * TILE;    // 2 stages
   static constexpr int BYTES = V + 2 * TILE;
-  static_assert(kDqWaves * 32 * D * 2 <= BYTES, "epilogue staging");
+  static_assert(kDqWaves * 32 * P * 2 <= BYTES, "epilogue staging");
 };
 
 template <int D, bool CAUSAL>
 __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
   using Tile = AsyncTile<D, kDqWaves>;
   using SM = DqSmem<D>;
+  constexpr int P = SM::P;
   __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
 
   const int tid = threadIdx.x;
@@ -190,7 +192,7 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
         }
 #pragma unroll
         for (int c = 0; c < D / 16; ++c) {
-          const int o = rr.rm[c] + 32 * kb * D;
+          const int o = rr.rm[c] + 32 * kb * P;
           s = mfma32(ld16(kc + o), qreg[c], s);
           dp = mfma32(ld16(vc + o), doreg[c], dp);
         }
@@ -210,7 +212,7 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
           const u32x4 b = pack_chunk(s, c);
-          const int rc = 16 * (2 * kb + c) * D;
+          const int rc = 16 * (2 * kb + c) * P;
 #pragma unroll
           for (int db = 0; db < D / 32; ++db) {
             const u32x2 lo = ld_tr(kc + trr.tr[db][0] + rc), hi = ld_tr(kc + trr.tr[db][1] + rc);
@@ -256,14 +258,14 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
     // region, 16-byte chunks swizzled by row), then written out as whole
     // rows (coalesced 16-byte stores).
     __syncthreads();   // every wavefront is done with the stages
-    uint16_t* stg = reinterpret_cast<uint16_t*>(smem + wave * 32 * D * 2);
-    const int sw = tile_swz<D>(l32);
+    uint16_t* stg = reinterpret_cast<uint16_t*>(smem + wave * 32 * P * 2);
+    const int sw = tile_swz<P>(l32);
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x16& v = dqacc[db];
-        st8(stg + l32 * D + 8 * ((4 * db + g) ^ sw) + 4 * half,
+        st8(stg + l32 * P + 8 * ((4 * db + g) ^ sw) + 4 * half,
             u32x2{pack_bf16(v[4 * g] * scale, v[4 * g + 1] * scale),
                   pack_bf16(v[4 * g + 2] * scale, v[4 * g + 3] * scale)});
       }
@@ -273,7 +275,7 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
     for (int i = 0; i < 32 * CPR / 64; ++i) {
       const int pidx = i * 64 + lane;
       const int row = pidx / CPR, ch = pidx % CPR;
-      const u32x4 v = ld16(stg + row * D + 8 * (ch ^ tile_swz<D>(row)));
+      const u32x4 v = ld16(stg + row * P + 8 * (ch ^ tile_swz<P>(row)));
       if (qw0 + row < len) st16(dqp + (int64_t)(qw0 + row) * q_row + 8 * ch, v);
     }
   }
@@ -285,7 +287,8 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
 // A workgroup covers 128 keys, 32 per wavefront group.  K and V of the
 // workgroup's keys stay in LDS (read as B operands) and the query-side tiles
 // (Q, dO, L log2 e, Delta) stream through two LDS stages.
-//  * D = 128: eight wavefronts; wavefronts w and w + 4 (which share a SIMD)
+//  * D = 128 and D = 96 (rows padded to 128 elements in LDS): eight
+//    wavefronts; wavefronts w and w + 4 (which share a SIMD)
 //    own the same 32 keys and take the two 32-query halves of every 64-query
 //    tile, and their two partial dK/dV accumulators are added through LDS at
 //    the end (one workgroup per CU: 129 KiB of LDS).
@@ -299,7 +302,8 @@ constexpr int dkv_waves() { return D == 64 ? 4 : 8; }
 
 template <int D>
 struct DkvSmem {
-  static constexpr int TILE = 64 * D * 2;                  // bytes of a 64-row bf16 tile
+  static constexpr int P = lds_pitch<D>();                 // LDS row pitch (elements)
+  static constexpr int TILE = 64 * P * 2;                  // bytes of a 64-row bf16 tile
   static constexpr int K = 0;                              // 2 tiles: keys 0-63, 64-127
   static constexpr int V = K + 2 * TILE;
   static constexpr int Q = V + 2 * TILE;                   // 2 stages
@@ -310,7 +314,7 @@ struct DkvSmem {
   // epilogue: one tensor's fp32 partial per wavefront (pairs), or the bf16
   // dK and dV rows of each wavefront
   static_assert(dkv_waves<D>() * (D / 32) * 4 * 1024 <= BYTES, "reduction buffer");
-  static_assert(dkv_waves<D>() * 2 * 32 * D * 2 <= BYTES, "epilogue staging");
+  static_assert(dkv_waves<D>() * 2 * 32 * P * 2 <= BYTES, "epilogue staging");
 };
 
 template <int D, bool CAUSAL>
@@ -319,6 +323,7 @@ __global__ __launch_bounds__(64 * dkv_waves<D>(), D == 64 ? 2 : 1) void bwd_dkdv
   constexpr bool PAIRS = NW == 8;   // two wavefronts per key group
   using Tile = AsyncTile<D, NW>;
   using SM = DkvSmem<D>;
+  constexpr int P = SM::P;
   __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
   uint16_t* const sk = reinterpret_cast<uint16_t*>(smem + SM::K);
   uint16_t* const sv = reinterpret_cast<uint16_t*>(smem + SM::V);
@@ -405,8 +410,8 @@ __global__ __launch_bounds__(64 * dkv_waves<D>(), D == 64 ? 2 : 1) void bwd_dkdv
     }
 
   // This wavefront's K and V rows: tile kq / 2, rows 32 (kq % 2) + l32.
-  const uint16_t* const krd = sk + (kq >> 1) * (SM::TILE / 2) + 32 * (kq & 1) * D;
-  const uint16_t* const vrd = sv + (kq >> 1) * (SM::TILE / 2) + 32 * (kq & 1) * D;
+  const uint16_t* const krd = sk + (kq >> 1) * (SM::TILE / 2) + 32 * (kq & 1) * P;
+  const uint16_t* const vrd = sv + (kq >> 1) * (SM::TILE / 2) + 32 * (kq & 1) * P;
 
   // Query half hq (32 queries) of tile n, in stage st, against this
   // wavefront's 32 keys.
@@ -425,7 +430,7 @@ __global__ __launch_bounds__(64 * dkv_waves<D>(), D == 64 ? 2 : 1) void bwd_dkdv
     }
 #pragma unroll
     for (int c = 0; c < D / 16; ++c) {
-      const int o = rr.rm[c] + 32 * hq * D;
+      const int o = rr.rm[c] + 32 * hq * P;
       s = mfma32(ld16(q + o), ld16(krd + rr.rm[c]), s);
       dp = mfma32(ld16(dout + o), ld16(vrd + rr.rm[c]), dp);
     }
@@ -450,7 +455,7 @@ __global__ __launch_bounds__(64 * dkv_waves<D>(), D == 64 ? 2 : 1) void bwd_dkdv
     for (int c = 0; c < 2; ++c) {
       const u32x4 pb = pack_chunk(s, c);
       const u32x4 dsb = pack_chunk(dp, c);
-      const int rc = 16 * (2 * hq + c) * D;
+      const int rc = 16 * (2 * hq + c) * P;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
         const u32x2 dlo = ld_tr(dout + trr.tr[db][0] + rc), dhi = ld_tr(dout + trr.tr[db][1] + rc);
@@ -494,12 +499,12 @@ __global__ __launch_bounds__(64 * dkv_waves<D>(), D == 64 ? 2 : 1) void bwd_dkdv
   const int64_t kv_row = L.kv_row;
   auto store_rows = [&](const f32x16 (&acc)[D / 32], float mul, uint16_t* stg, uint16_t* gout)
       __attribute__((always_inline)) {
-    const int sw = tile_swz<D>(l32);
+    const int sw = tile_swz<P>(l32);
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int g = 0; g < 4; ++g)
-        st8(stg + l32 * D + 8 * ((4 * db + g) ^ sw) + 4 * half,
+        st8(stg + l32 * P + 8 * ((4 * db + g) ^ sw) + 4 * half,
             u32x2{pack_bf16(acc[db][4 * g] * mul, acc[db][4 * g + 1] * mul),
                   pack_bf16(acc[db][4 * g + 2] * mul, acc[db][4 * g + 3] * mul)});
     constexpr int CPR = D / 8;
@@ -507,15 +512,15 @@ __global__ __launch_bounds__(64 * dkv_waves<D>(), D == 64 ? 2 : 1) void bwd_dkdv
     for (int i = 0; i < 32 * CPR / 64; ++i) {
       const int pidx = i * 64 + lane;
       const int row = pidx / CPR, ch = pidx % CPR;
-      const u32x4 v = ld16(stg + row * D + 8 * (ch ^ tile_swz<D>(row)));
+      const u32x4 v = ld16(stg + row * P + 8 * (ch ^ tile_swz<P>(row)));
       if (kw0 + row < len) st16(gout + (int64_t)(kw0 + row) * kv_row + 8 * ch, v);
     }
   };
   if constexpr (!PAIRS) {
     // Each wavefront holds the whole of its keys' dK and dV.
-    uint16_t* stg = reinterpret_cast<uint16_t*>(smem) + wave * 2 * 32 * D;
+    uint16_t* stg = reinterpret_cast<uint16_t*>(smem) + wave * 2 * 32 * P;
     store_rows(dkacc, a.scale, stg, a.dk + kvoff);
-    store_rows(dvacc, 1.f, stg + 32 * D, a.dv + kvoff);
+    store_rows(dvacc, 1.f, stg + 32 * P, a.dv + kvoff);
   } else {
     // The pair splits the work: the sb = 0 wavefront finalises dK, the
     // sb = 1 one dV.  Each first hands its partial of the other tensor to
@@ -560,45 +565,49 @@ __global__ __launch_bounds__(64 * dkv_waves<D>(), D == 64 ? 2 : 1) void bwd_dkdv
 // launch stubs of these templates (leaving undefined symbols in the library).
 template __global__ void bwd_dq_kernel<64, false>(BwdArgs);
 template __global__ void bwd_dq_kernel<64, true>(BwdArgs);
+template __global__ void bwd_dq_kernel<96, false>(BwdArgs);
+template __global__ void bwd_dq_kernel<96, true>(BwdArgs);
 template __global__ void bwd_dq_kernel<128, false>(BwdArgs);
 template __global__ void bwd_dq_kernel<128, true>(BwdArgs);
 template __global__ void bwd_dkdv_kernel<64, false>(BwdArgs);
 template __global__ void bwd_dkdv_kernel<64, true>(BwdArgs);
+template __global__ void bwd_dkdv_kernel<96, false>(BwdArgs);
+template __global__ void bwd_dkdv_kernel<96, true>(BwdArgs);
 template __global__ void bwd_dkdv_kernel<128, false>(BwdArgs);
 template __global__ void bwd_dkdv_kernel<128, true>(BwdArgs);
 
 }  // namespace
 
-hipError_t launch_bwd(const BwdArgs& a, int D, int phases, hipStream_t stream) {
+namespace {
+
+template <int D>
+void launch_bwd_d(const BwdArgs& a, int phases, hipStream_t stream) {
   // A dQ workgroup takes a query block and its mirror (see the kernel).
   const dim3 gq((unsigned)(a.L.nseg * a.L.Hq), (unsigned)(((a.L.S + kQM - 1) / kQM + 1) / 2));
   const dim3 gk((unsigned)(a.L.nseg * a.L.Hkv), (unsigned)((a.L.S + kKN - 1) / kKN));
   if (phases & 1) {
-    if (D == 64) {
-      if (a.causal)
-        hipLaunchKernelGGL((bwd_dq_kernel<64, true>), gq, dim3(kDqThreads), 0, stream, a);
-      else
-        hipLaunchKernelGGL((bwd_dq_kernel<64, false>), gq, dim3(kDqThreads), 0, stream, a);
-    } else {
-      if (a.causal)
-        hipLaunchKernelGGL((bwd_dq_kernel<128, true>), gq, dim3(kDqThreads), 0, stream, a);
-      else
-        hipLaunchKernelGGL((bwd_dq_kernel<128, false>), gq, dim3(kDqThreads), 0, stream, a);
-    }
+    if (a.causal)
+      hipLaunchKernelGGL((bwd_dq_kernel<D, true>), gq, dim3(kDqThreads), 0, stream, a);
+    else
+      hipLaunchKernelGGL((bwd_dq_kernel<D, false>), gq, dim3(kDqThreads), 0, stream, a);
   }
   if (phases & 2) {
-    if (D == 64) {
-      if (a.causal)
-        hipLaunchKernelGGL((bwd_dkdv_kernel<64, true>), gk, dim3(64 * dkv_waves<64>()), 0, stream, a);
-      else
-        hipLaunchKernelGGL((bwd_dkdv_kernel<64, false>), gk, dim3(64 * dkv_waves<64>()), 0, stream, a);
-    } else {
-      if (a.causal)
-        hipLaunchKernelGGL((bwd_dkdv_kernel<128, true>), gk, dim3(64 * dkv_waves<128>()), 0, stream, a);
-      else
-        hipLaunchKernelGGL((bwd_dkdv_kernel<128, false>), gk, dim3(64 * dkv_waves<128>()), 0, stream, a);
-    }
+    if (a.causal)
+      hipLaunchKernelGGL((bwd_dkdv_kernel<D, true>), gk, dim3(64 * dkv_waves<D>()), 0, stream, a);
+    else
+      hipLaunchKernelGGL((bwd_dkdv_kernel<D, false>), gk, dim3(64 * dkv_waves<D>()), 0, stream, a);
   }
+}
+
+}  // namespace
+
+hipError_t launch_bwd(const BwdArgs& a, int D, int phases, hipStream_t stream) {
+  if (D == 64)
+    launch_bwd_d<64>(a, phases, stream);
+  else if (D == 96)
+    launch_bwd_d<96>(a, phases, stream);
+  else
+    launch_bwd_d<128>(a, phases, stream);
   return hipGetLastError();
 }
 

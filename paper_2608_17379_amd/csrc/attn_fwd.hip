@@ -35,13 +35,15 @@ constexpr int kBM = 128;   // query rows per workgroup
 constexpr int kBN = 64;    // keys per iteration
 constexpr float kRescaleSlack = 8.0f;   // log2 of the largest P entry allowed
 
-// Two LDS stages (2 x 32 KiB at D = 128: two workgroups per CU), declared as
+// Two LDS stages (2 x 32 KiB at D = 128 and at D = 96, whose rows are padded
+// to 128 elements; two workgroups per CU), declared as
 // separate objects so that the compiler can tell a stage being filled by DMA
 // from the one being read and does not wait for the prefetch.
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   using Tile = AsyncTile<D>;
+  constexpr int P = Tile::P;   // LDS row pitch (elements)
   __shared__ __attribute__((aligned(1024))) uint16_t sk0[Tile::ELEMS];
   __shared__ __attribute__((aligned(1024))) uint16_t sk1[Tile::ELEMS];
   __shared__ __attribute__((aligned(1024))) uint16_t sv0[Tile::ELEMS];
@@ -122,7 +124,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
       for (int c = 0; c < D / 16; ++c)
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
-          s[kb] = mfma32(ld16(kt_lds + kr.rm[c] + 32 * kb * D), qreg[c], s[kb]);
+          s[kb] = mfma32(ld16(kt_lds + kr.rm[c] + 32 * kb * P), qreg[c], s[kb]);
 
       // s[kb][r] is the raw score of key k0 + 32kb + 8(r/4) + 4half + r%4.
       if ((a.causal && k0 + kBN - 1 > qw0) || k0 + kBN > seg.len) {
@@ -171,8 +173,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
         const u32x4 pb = pack_chunk(s[c >> 1], c & 1);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
-          const u32x2 lo = ld_tr(vt_lds + vr.tr[db][0] + 16 * c * D);
-          const u32x2 hi = ld_tr(vt_lds + vr.tr[db][1] + 16 * c * D);
+          const u32x2 lo = ld_tr(vt_lds + vr.tr[db][0] + 16 * c * P);
+          const u32x2 hi = ld_tr(vt_lds + vr.tr[db][1] + 16 * c * P);
           oacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb, oacc[db]);
         }
       }
@@ -237,6 +239,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
 // Explicit instantiations: without them the host compiler may skip the
 // launch stubs of these templates (leaving undefined symbols in the library).
 template __global__ void fwd_kernel<64>(FwdArgs);
+template __global__ void fwd_kernel<96>(FwdArgs);
 template __global__ void fwd_kernel<128>(FwdArgs);
 
 }  // namespace
@@ -247,6 +250,8 @@ hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream) {
   const dim3 grid((unsigned)(a.L.nseg * a.L.Hq), (unsigned)((nqt + 1) / 2));
   if (D == 64)
     hipLaunchKernelGGL(fwd_kernel<64>, grid, dim3(kThreads), 0, stream, a);
+  else if (D == 96)
+    hipLaunchKernelGGL(fwd_kernel<96>, grid, dim3(kThreads), 0, stream, a);
   else
     hipLaunchKernelGGL(fwd_kernel<128>, grid, dim3(kThreads), 0, stream, a);
   return hipGetLastError();

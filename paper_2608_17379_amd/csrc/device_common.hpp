@@ -91,16 +91,17 @@ __device__ __forceinline__ rsrc_t rows_rsrc(const uint16_t* head_base, int row0,
 }
 
 // ---------------------------------------------------------------------------
-// Asynchronous tiles: [64 rows][D] bf16 tiles filled straight from global
-// memory into LDS (buffer_load ... lds) and read back either row-major
-// (16-byte MFMA operand rows) or transposed (ds_read_b64_tr_b16).  gfx950's
-// LDS serves 64 banks x 4 bytes: a 16-byte access 16 lanes at a time, an
-// 8-byte access 32 lanes at a time.
+// Asynchronous tiles: [64 rows][P] bf16 tiles (P = lds_pitch<D>() elements
+// per row, D of them used) filled straight from global memory into LDS
+// (buffer_load ... lds) and read back either row-major (16-byte MFMA operand
+// rows) or transposed (ds_read_b64_tr_b16).  gfx950's LDS serves 64 banks x
+// 4 bytes: a 16-byte access 16 lanes at a time, an 8-byte access 32 lanes at
+// a time.
 //
 // A DMA load writes 16 bytes per lane to consecutive LDS addresses (lane L
 // of the wave at base + 16 L), so the layout is chosen by which source chunk
-// each lane fetches: LDS granule p holds row p / (D/8), logical 16-byte chunk
-// (p % (D/8)) ^ tile_swz<D>(row).  The swizzle makes both read patterns hit
+// each lane fetches: LDS granule p holds row p / (P/8), logical 16-byte chunk
+// (p % (P/8)) ^ tile_swz<P>(row).  The swizzle makes both read patterns hit
 // 64 distinct banks per access phase: sixteen consecutive rows at one chunk
 // (row-major reads), and four consecutive rows x four chunks (transposed
 // reads).
@@ -108,19 +109,36 @@ __device__ __forceinline__ rsrc_t rows_rsrc(const uint16_t* head_base, int row0,
 #define ATTN_LDS __attribute__((address_space(3)))
 typedef __attribute__((ext_vector_type(4))) short s16x4;
 
+// LDS row pitch (elements) of a tile whose rows hold D values: rows of
+// D = 96 are padded to 128 elements, so that they use the 16-chunk swizzle
+// below; chunks 12..15 of such rows are never read.
 template <int D>
+constexpr int lds_pitch() {
+  static_assert(D == 64 || D == 96 || D == 128, "head dimension");
+  return D == 96 ? 128 : D;
+}
+
+// Swizzle of the 16-byte chunks of row r of a tile with pitch P elements.
+template <int P>
 __device__ __forceinline__ int tile_swz(int r) {
-  if constexpr (D == 128)
+  static_assert(P == 64 || P == 128, "tile pitch");
+  if constexpr (P == 128)
     return ((r & 3) << 2) | ((r >> 2) & 3);
   else
     return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
 }
 
+// Byte offset given to the DMA lanes of the pad chunks of a padded row: far
+// beyond any buffer's range (at most 2^31 - 1 bytes), so the hardware range
+// check turns the load into zeros without a memory access.
+constexpr int kPadOffset = (int)0xFFFFFF00u;
+
 template <int D, int NW = 4>
 struct AsyncTile {
-  static constexpr int CPR = D / 8;          // 16-byte chunks per row
+  static constexpr int P = lds_pitch<D>();   // LDS row pitch (elements)
+  static constexpr int CPR = P / 8;          // 16-byte chunks per LDS row
   static constexpr int NJ = CPR / NW;        // DMA instructions per wavefront (64 rows)
-  static constexpr int ELEMS = 64 * D;       // bf16 elements per tile
+  static constexpr int ELEMS = 64 * P;       // bf16 elements per tile
   static_assert(NJ * NW * 64 == 64 * CPR, "tile split");
   int goff[NJ];                              // this lane's source byte offset per instruction
   __device__ __forceinline__ AsyncTile(int wave, int lane, int row_bytes) {
@@ -128,8 +146,8 @@ struct AsyncTile {
     for (int j = 0; j < NJ; ++j) {
       const int p = (wave * NJ + j) * 64 + lane;
       const int row = p / CPR;
-      const int logical = (p % CPR) ^ tile_swz<D>(row);
-      goff[j] = row * row_bytes + 16 * logical;
+      const int logical = (p % CPR) ^ tile_swz<P>(row);
+      goff[j] = logical < D / 8 ? row * row_bytes + 16 * logical : kPadOffset;
     }
   }
   // Enqueue this wavefront's share of a tile: rows [0, 64) of `src` into
@@ -143,14 +161,15 @@ struct AsyncTile {
 };
 
 // Row-major read offsets (elements) of an MFMA operand over rows
-// 32*b + (lane % 32), 16-byte chunk 2c + half: rm[c] + 32*b*D.
+// 32*b + (lane % 32), 16-byte chunk 2c + half: rm[c] + 32*b*P.
 template <int D>
 struct RowReader {
+  static constexpr int P = lds_pitch<D>();
   int rm[D / 16];
   __device__ __forceinline__ RowReader(int l32, int half) {
-    const int x = tile_swz<D>(l32);
+    const int x = tile_swz<P>(l32);
 #pragma unroll
-    for (int c = 0; c < D / 16; ++c) rm[c] = l32 * D + 8 * ((2 * c + half) ^ x);
+    for (int c = 0; c < D / 16; ++c) rm[c] = l32 * P + 8 * ((2 * c + half) ^ x);
   }
 };
 
@@ -158,11 +177,12 @@ struct RowReader {
 // column of the tile (d) and whose reduction index runs over tile rows.  For
 // column block db and 16-row chunk c, lane (l32, half) receives rows
 // 16c + 8(e/4) + 4 half + e%4 (e = 0..7) of column 32 db + l32, as two
-// ds_read_b64_tr_b16 at tr[db][0] + 16 c D and tr[db][1] + 16 c D.
+// ds_read_b64_tr_b16 at tr[db][0] + 16 c P and tr[db][1] + 16 c P.
 // (Within each 16-lane group, transposed read lane i returns element i % 4
 // of the 8 bytes addressed by lanes 4e + i/4, e = 0..3.)
 template <int D>
 struct TransReader {
+  static constexpr int P = lds_pitch<D>();
   int tr[D / 32][2];
   __device__ __forceinline__ TransReader(int lane) {
     const int grp = lane >> 4, j = lane & 15;
@@ -172,8 +192,8 @@ struct TransReader {
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
         const int row = 8 * hh + 4 * h + e;
-        const int phys = (4 * db + 2 * g + (m >> 1)) ^ tile_swz<D>(row);
-        tr[db][hh] = row * D + 8 * phys + 4 * (m & 1);
+        const int phys = (4 * db + 2 * g + (m >> 1)) ^ tile_swz<P>(row);
+        tr[db][hh] = row * P + 8 * phys + 4 * (m & 1);
       }
   }
 };

@@ -15,9 +15,11 @@ Shapes follow the attention workloads of PTXBench (Appendix A, "Workloads"
 and "Generalization attention workloads"): bf16 Q, K, V of shape
 [B, H, S, D], an fp32 log-sum-exp of shape [B, H, S], causal variants with a
 lower-triangular mask, grouped-query variants with fewer key/value heads, and
-ragged causal prefill over packed sequences.  The five sizes below are the
-ones this library is measured on; the paper's own trace files are not
-available, so these synthetic tensors stand in for them.
+ragged causal prefill over packed sequences.  The sizes below are the ones this
+library is measured on; the paper's own trace files are not available, so
+these synthetic tensors stand in for them.  The paper gives the ragged
+prefill workload only as a sequence count and a token total, so its lengths
+are drawn as a uniformly random composition of the total.
 """
 from __future__ import annotations
 
@@ -41,6 +43,8 @@ class Workload:
     varlen: bool = False
     len_lo: int = 0   # packed: lengths drawn uniformly in [len_lo, len_hi]
     len_hi: int = 0
+    total: int = 0    # packed: if > 0, lengths are a random composition of
+                      # `total` into B positive parts instead
 
     @property
     def scale(self) -> float:
@@ -58,6 +62,16 @@ WORKLOADS = {
     "varlen_causal_n8_l512_8192_h32_d64": Workload(
         "varlen_causal_n8_l512_8192_h32_d64", 8, 32, 32, 8192, 64, True,
         varlen=True, len_lo=512, len_hi=8192),
+    # The paper's own attention shape (B4 H48 S4096), at its three head
+    # dimensions, non-causal and causal.
+    **{f"mha{c}_b4_h48_s4096_d{d}": Workload(f"mha{c}_b4_h48_s4096_d{d}", 4, 48, 48, 4096, d,
+                                             c == "_causal")
+       for d in (64, 96, 128) for c in ("", "_causal")},
+    # The paper's ragged causal prefill: 33 sequences, 16,294 tokens in all,
+    # 32 query heads over 4 key/value heads, D = 128.
+    "ragged_gqa_causal_n33_t16294_hq32_hkv4_d128": Workload(
+        "ragged_gqa_causal_n33_t16294_hq32_hkv4_d128", 33, 32, 4, 16294, 128, True,
+        varlen=True, total=16294),
 }
 
 # The configuration the headline throughput is quoted on.
@@ -85,6 +99,17 @@ class Inputs:
         return max(b - a for a, b in zip(cu, cu[1:]))
 
 
+def random_composition(gen: torch.Generator, total: int, parts: int) -> List[int]:
+    """`parts` positive lengths summing to `total`, uniform over all such
+    compositions: the gaps between `parts - 1` distinct cut points drawn
+    without replacement from 1 .. total - 1."""
+    if parts < 1 or total < parts:
+        raise ValueError("need total >= parts >= 1")
+    cuts = (torch.randperm(total - 1, generator=gen)[:parts - 1] + 1).sort().values.tolist()
+    bounds = [0] + cuts + [total]
+    return [b - a for a, b in zip(bounds, bounds[1:])]
+
+
 def _randn_bf16(gen: torch.Generator, shape) -> torch.Tensor:
     return torch.randn(*shape, generator=gen, dtype=torch.float32).to(torch.bfloat16)
 
@@ -97,7 +122,9 @@ def make_inputs(w: Workload, seed: int = 0, lengths: Optional[List[int]] = None)
     """
     gen = torch.Generator().manual_seed(seed)
     if w.varlen:
-        if lengths is None:
+        if lengths is None and w.total:
+            lengths = random_composition(gen, w.total, w.B)
+        elif lengths is None:
             lengths = torch.randint(w.len_lo, w.len_hi + 1, (w.B,), generator=gen).tolist()
         cu = [0]
         for n in lengths:

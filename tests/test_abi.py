@@ -78,7 +78,8 @@ def test_scalar_validation(call):
     assert call(Hq=0) == -2
     assert call(Hkv=0) == -2
     assert call(Hq=3, Hkv=2) == -3
-    assert call(D=96) == -4
+    assert call(D=80) == -4
+    assert call(D=32) == -4
     assert call(D=256) == -4
     assert call(causal=2) == -8
     assert call(scale=float("nan")) == -8

@@ -2,9 +2,9 @@
 
 Small shapes are compared element by element over whole tensors and span
 several tiles plus ragged tails (tiles are 128 query rows x 64 keys forward,
-128 keys x 64 queries for dK/dV).  The five measured workloads run at full
-size in the benchmark's launch configuration and are compared on sampled
-heads, which the oracle computes exactly (head slices are independent
+128 keys x 64 queries for dK/dV), at head dimensions 64, 96 and 128.  The
+measured workloads run at full size in the benchmark's launch configuration
+and are compared on sampled heads, which the oracle computes exactly (head slices are independent
 problems: one query head for O, LSE and dQ, one key/value head with its whole
 query-head group for dK and dV).
 """
@@ -40,21 +40,21 @@ def test_smallest_workload_exact_shape():
     check_all(gpu_fwd_bwd(x, w.causal, w.scale), oracle_all(x, w.causal, w.scale), w.name)
 
 
-@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("D", [64, 96, 128])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("S", [1, 2, 17, 63, 64, 65, 127, 128, 129, 200, 383])
 def test_shapes_mha(S, D, causal):
     _fixed_case(S, D, causal)
 
 
-@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("D", [64, 96, 128])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("Hq,Hkv", [(4, 2), (8, 2), (8, 1)])
 def test_shapes_gqa(Hq, Hkv, D, causal):
     _fixed_case(190, D, causal, Hq=Hq, Hkv=Hkv, B=2)
 
 
-@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("D", [64, 96, 128])
 def test_long_ragged_sequence(D):
     _fixed_case(1000, D, True, Hq=2, Hkv=1)
 
@@ -63,7 +63,7 @@ def test_peaky_rows():
     _fixed_case(300, 128, True, qk_mult=4.0)
 
 
-@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("D", [64, 96, 128])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("Hq,Hkv", [(2, 2), (4, 1)])
 def test_packed_ragged(D, causal, Hq, Hkv):
@@ -205,3 +205,15 @@ def test_full_long_causal_b1_h16_s16384_d128_qk2():
 
 def test_full_varlen_causal_n8_l512_8192_h32_d64():
     _full_size("varlen_causal_n8_l512_8192_h32_d64", [(0, 0), (3, 31), (7, 12)])
+
+
+@pytest.mark.parametrize("name", [f"mha{c}_b4_h48_s4096_d{d}" for d in (64, 96, 128)
+                                  for c in ("", "_causal")])
+def test_full_paper_shape(name):
+    _full_size(name, [(0, 0), (3, 47)])
+
+
+def test_full_ragged_gqa_causal_n33_t16294_hq32_hkv4_d128():
+    # The shortest (5 rows), a middle (719) and the longest (1372) sequence of
+    # the seeded draw, each with a whole key/value head group.
+    _full_size("ragged_gqa_causal_n33_t16294_hq32_hkv4_d128", [(27, 0), (14, 3), (28, 1)])

@@ -425,6 +425,17 @@ def test_workload_inputs_are_seeded_and_shaped():
     assert x.max_seqlen == 17
 
 
+def test_ragged_prefill_lengths_are_a_composition():
+    """33 positive lengths summing to 16,294 tokens, the same for a seed."""
+    w = wl.WORKLOADS["ragged_gqa_causal_n33_t16294_hq32_hkv4_d128"]
+    gen = torch.Generator().manual_seed(0)
+    lens = wl.random_composition(gen, w.total, w.B)
+    assert len(lens) == 33 and sum(lens) == 16294 and min(lens) >= 1
+    assert lens == wl.random_composition(torch.Generator().manual_seed(0), w.total, w.B)
+    assert wl.random_composition(torch.Generator().manual_seed(1), 5, 5) == [1] * 5
+    assert wl.random_composition(torch.Generator().manual_seed(1), 7, 1) == [7]
+
+
 def test_oracle_regression_fixture():
     """Oracle output on the smallest workload equals the committed fixture."""
     import json

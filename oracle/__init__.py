@@ -6,7 +6,8 @@ the benchmark may use it.  It shares no code with the HIP library.
 
 The oracle is the plain definition of attention (whole-row two-pass softmax in
 fp64), not the tiled online-softmax method the GPU runs.  Every function is
-pinned by the CPU tests in ``tests/test_oracle.py`` against closed forms,
+pinned by the CPU tests in ``tests/test_oracle.py`` and
+``tests/test_oracle_paged.py`` against closed forms,
 invariants, finite differences, a pure-Python brute force and torch's own fp64
 SDPA; no function is left "parity unpinned".
 """
@@ -15,5 +16,7 @@ from .attention import (
     attention_backward,
     attention_probs,
 )
+from .paged import attention_forward_paged
 
-__all__ = ["attention_forward", "attention_backward", "attention_probs"]
+__all__ = ["attention_forward", "attention_backward", "attention_probs",
+           "attention_forward_paged"]

@@ -70,13 +70,17 @@ def _softmax_rows(x: torch.Tensor):
     return p, lse.squeeze(1)
 
 
-def _head_forward(qh, kh, vh, causal, scale, block_rows):
+def _head_forward(qh, kh, vh, causal, scale, block_rows, pos0=0):
+    """One query head.  Query row i sits at key position pos0 + i (0 unless
+    the queries are the last rows of a longer key sequence)."""
     n = qh.shape[0]
     o = torch.zeros(n, vh.shape[1], dtype=_F64)
     lse = torch.full((n,), -math.inf, dtype=_F64)
+    if kh.shape[0] == 0:   # no keys at all: every row is empty
+        return o, lse
     for r0 in range(0, n, block_rows):
         r1 = min(n, r0 + block_rows)
-        p, l = _softmax_rows(_scores(qh[r0:r1], kh, r0, causal, scale))
+        p, l = _softmax_rows(_scores(qh[r0:r1], kh, pos0 + r0, causal, scale))
         o[r0:r1] = p @ vh
         lse[r0:r1] = l
     return o, lse

@@ -61,13 +61,15 @@ typedef enum {
   ATTN_ERR_NULL = -1,       /* a required pointer is null */
   ATTN_ERR_SHAPE = -2,      /* a size is negative, Hq/Hkv < 1, or too large
                                (S or max_seqlen > 65535*128, Hq*D > 2^22) */
-  ATTN_ERR_GQA = -3,        /* Hq is not a multiple of Hkv */
+  ATTN_ERR_GQA = -3,        /* Hq is not a multiple of Hkv, or (decode)
+                               Hq / Hkv > 32 */
   ATTN_ERR_HEAD_DIM = -4,   /* D is not 64, 96 or 128 */
   ATTN_ERR_ALIGN = -5,      /* a pointer is not 16-byte aligned */
   ATTN_ERR_WORKSPACE = -6,  /* workspace null or smaller than required */
   ATTN_ERR_HIP = -7,        /* a kernel launch failed (hipGetLastError) */
   ATTN_ERR_VALUE = -8       /* scale not finite or not > 0, causal not 0/1,
-                               max_seqlen < 1, or a bad backward phase mask */
+                               max_seqlen (max_qlen, max_kvlen) < 1, or a bad
+                               backward phase mask */
 } attn_status_t;
 
 /*
@@ -144,6 +146,64 @@ int attn_bwd_varlen_phases(const void* q, const void* k, const void* v,
                            float scale, void* workspace,
                            size_t workspace_bytes, int phases,
                            hipStream_t stream);
+
+/*
+ * Paged key/value cache, page size 1 (the paged causal prefill and paged
+ * decode workloads of PTXBench, Appendix A, "Generalization attention
+ * workloads"; forward only, as there).
+ *
+ *   k_cache, v_cache  [num_pages, Hkv, D] bf16: one token per page.
+ *   kv_indptr         int32 [batch+1], non-decreasing, from 0 to nnz.
+ *   kv_indices        int32 [nnz]: request b's keys and values are the pages
+ *                     kv_indices[kv_indptr[b]] .. kv_indices[kv_indptr[b+1]-1],
+ *                     in that order (kv_len_b of them).
+ *
+ * Attention of each request's queries over its keys, as for the packed
+ * layout.  When a request has q_len queries and kv_len keys, its queries are
+ * the last q_len of its kv_len positions: with the causal mask, query i
+ * (0-based within the request) sees keys j <= i + kv_len - q_len (the
+ * lower-triangular mask when q_len == kv_len).  Rows that see no key get
+ * O = 0 and lse = -inf.
+ *
+ * The library reads the index arrays only on the device: offsets are clamped
+ * into [0, nnz] and a page number outside [0, num_pages) reads as a zero key
+ * and value row, so bad contents cannot make a kernel access memory outside
+ * the given arrays (the results are then meaningless; the Python binding
+ * checks the arrays on the host).  num_pages * Hkv * D * 2 must be below
+ * 2^31 and nnz at most 2^29 (ATTN_ERR_SHAPE).  The index arrays need 4-byte
+ * alignment, every other pointer 16-byte alignment.
+ */
+
+/*
+ * Paged prefill.  q, o [total_q, Hq, D] packed by qo_indptr (int32 [batch+1],
+ * from 0 to total_q, as cu_seqlens); lse [Hq, total_q] fp32.  max_qlen >= the
+ * longest query run (it sizes the launch).  causal 0 or 1.
+ */
+int attn_fwd_paged(const void* q, const void* k_cache, const void* v_cache, void* o,
+                   float* lse, const int* qo_indptr, const int* kv_indptr,
+                   const int* kv_indices, int batch, int max_qlen, int total_q, int nnz,
+                   int num_pages, int Hq, int Hkv, int D, int causal, float scale,
+                   hipStream_t stream);
+
+/* Bytes of workspace for attn_decode_paged (partial outputs of the key
+ * chunks: fp32 [batch, Hq, ceil(max_kvlen / 128), D + 1], rounded up). */
+size_t attn_decode_paged_workspace_size(int batch, int max_kvlen, int Hq, int Hkv, int D);
+
+/*
+ * Paged decode: one query per request.  q, o [batch, Hq, D]; lse [Hq, batch]
+ * fp32.  Every key of the request is visible.  max_kvlen >= the longest
+ * request (it sizes the launch and the workspace; a longer request is
+ * truncated to its first max_kvlen keys).  Hq / Hkv must be at most 32
+ * (ATTN_ERR_GQA).  The workspace (16-byte aligned, caller-owned, contents
+ * irrelevant) holds the partial results of the key chunks; calls that share
+ * a workspace must not overlap.  A request with no keys gets O = 0 and
+ * lse = -inf.
+ */
+int attn_decode_paged(const void* q, const void* k_cache, const void* v_cache, void* o,
+                      float* lse, const int* kv_indptr, const int* kv_indices, int batch,
+                      int max_kvlen, int nnz, int num_pages, int Hq, int Hkv, int D,
+                      float scale, void* workspace, size_t workspace_bytes,
+                      hipStream_t stream);
 
 /* Static, human-readable text for a status code (never null). */
 const char* attn_status_string(int status);

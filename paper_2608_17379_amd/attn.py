@@ -25,7 +25,8 @@ STATUS_NAMES = {
 }
 EXPORTS = ("attn_fwd", "attn_bwd", "attn_bwd_workspace_size", "attn_fwd_varlen",
            "attn_bwd_varlen", "attn_bwd_varlen_workspace_size", "attn_bwd_phases",
-           "attn_bwd_varlen_phases", "attn_status_string")
+           "attn_bwd_varlen_phases", "attn_fwd_paged", "attn_decode_paged_workspace_size",
+           "attn_decode_paged", "attn_status_string")
 ATTN_BWD_DQ = 1
 ATTN_BWD_DKDV = 2
 
@@ -63,6 +64,12 @@ def lib() -> ctypes.CDLL:
         l.attn_bwd_phases.restype = _I
         l.attn_bwd_varlen_phases.argtypes = [_P] * 10 + [_I] * 7 + [_F, _P, _Z, _I, _P]
         l.attn_bwd_varlen_phases.restype = _I
+        l.attn_fwd_paged.argtypes = [_P] * 8 + [_I] * 9 + [_F, _P]
+        l.attn_fwd_paged.restype = _I
+        l.attn_decode_paged_workspace_size.argtypes = [_I] * 5
+        l.attn_decode_paged_workspace_size.restype = _Z
+        l.attn_decode_paged.argtypes = [_P] * 7 + [_I] * 7 + [_F, _P, _Z, _P]
+        l.attn_decode_paged.restype = _I
         l.attn_status_string.argtypes = [_I]
         l.attn_status_string.restype = ctypes.c_char_p
         _lib = l
@@ -235,8 +242,108 @@ def attn_bwd_varlen(q, k, v, o, lse, dO, dq, dk, dv, cu_seqlens, max_seqlen: int
 
 
 # --------------------------------------------------------------------------
+# Paged key/value cache, page size 1 (forward only)
+# --------------------------------------------------------------------------
+
+def _host_list(t, host):
+    return [int(x) for x in (host if host is not None else t.cpu().tolist())]
+
+
+def check_paged_host(kv_host: Sequence[int], idx_host: Sequence[int], num_pages: int,
+                     max_kvlen: Optional[int] = None) -> None:
+    """Host-side check of the page arrays the library cannot read itself."""
+    if not kv_host or kv_host[0] != 0 or kv_host[-1] != len(idx_host):
+        raise ValueError("kv_indptr must start at 0 and end at len(kv_indices)")
+    if any(b < a for a, b in zip(kv_host, kv_host[1:])):
+        raise ValueError("kv_indptr must be non-decreasing")
+    if any(p < 0 or p >= num_pages for p in idx_host):
+        raise ValueError("a page index is outside the cache")
+    if max_kvlen is not None and any(b - a > max_kvlen for a, b in zip(kv_host, kv_host[1:])):
+        raise ValueError("a request has more than max_kvlen keys")
+
+
+def attn_fwd_paged(q, k_cache, v_cache, o, lse, qo_indptr, kv_indptr, kv_indices,
+                   max_qlen: int, causal: bool, scale: float, stream=None,
+                   qo_indptr_host=None, kv_indptr_host=None, kv_indices_host=None) -> None:
+    Tq, Hq, D = q.shape
+    P, Hkv = k_cache.shape[0], k_cache.shape[1]
+    _shape(k_cache, (P, Hkv, D), "k_cache")
+    _shape(v_cache, (P, Hkv, D), "v_cache")
+    _shape(o, (Tq, Hq, D), "o")
+    _shape(lse, (Hq, Tq), "lse")
+    batch = qo_indptr.numel() - 1
+    if kv_indptr.numel() != batch + 1:
+        raise ValueError("qo_indptr and kv_indptr must have the same length")
+    check_cu_seqlens(_host_list(qo_indptr, qo_indptr_host), Tq, max_qlen)
+    check_paged_host(_host_list(kv_indptr, kv_indptr_host),
+                     _host_list(kv_indices, kv_indices_host), P)
+    nnz = kv_indices.numel()
+    st = lib().attn_fwd_paged(_ptr(q, "q"), _ptr(k_cache, "k_cache"), _ptr(v_cache, "v_cache"),
+                              _ptr(o, "o"), _ptr(lse, "lse", torch.float32),
+                              _ptr(qo_indptr, "qo_indptr", torch.int32),
+                              _ptr(kv_indptr, "kv_indptr", torch.int32),
+                              _ptr(kv_indices, "kv_indices", torch.int32) if nnz else 0,
+                              batch, int(max_qlen), Tq, nnz, P, Hq, Hkv, D, int(bool(causal)),
+                              float(scale), _stream(stream))
+    _check(st, "attn_fwd_paged")
+
+
+def attn_decode_paged_workspace_size(batch: int, max_kvlen: int, Hq: int, Hkv: int, D: int) -> int:
+    return int(lib().attn_decode_paged_workspace_size(batch, max_kvlen, Hq, Hkv, D))
+
+
+def attn_decode_paged(q, k_cache, v_cache, o, lse, kv_indptr, kv_indices, max_kvlen: int,
+                      scale: float, workspace: torch.Tensor, stream=None,
+                      kv_indptr_host=None, kv_indices_host=None) -> None:
+    batch, Hq, D = q.shape
+    P, Hkv = k_cache.shape[0], k_cache.shape[1]
+    _shape(k_cache, (P, Hkv, D), "k_cache")
+    _shape(v_cache, (P, Hkv, D), "v_cache")
+    _shape(o, (batch, Hq, D), "o")
+    _shape(lse, (Hq, batch), "lse")
+    _shape(kv_indptr, (batch + 1,), "kv_indptr")
+    check_paged_host(_host_list(kv_indptr, kv_indptr_host),
+                     _host_list(kv_indices, kv_indices_host), P, max_kvlen)
+    nnz = kv_indices.numel()
+    st = lib().attn_decode_paged(_ptr(q, "q"), _ptr(k_cache, "k_cache"), _ptr(v_cache, "v_cache"),
+                                 _ptr(o, "o"), _ptr(lse, "lse", torch.float32),
+                                 _ptr(kv_indptr, "kv_indptr", torch.int32),
+                                 _ptr(kv_indices, "kv_indices", torch.int32) if nnz else 0,
+                                 batch, int(max_kvlen), nnz, P, Hq, Hkv, D, float(scale),
+                                 _ptr(workspace, "workspace", torch.uint8), workspace.numel(),
+                                 _stream(stream))
+    _check(st, "attn_decode_paged")
+
+
+# --------------------------------------------------------------------------
 # Allocating conveniences (torch allocates the outputs; the library fills them)
 # --------------------------------------------------------------------------
+
+def forward_paged(q, k_cache, v_cache, qo_indptr, kv_indptr, kv_indices, max_qlen: int,
+                  causal: bool, scale: float, **host):
+    """Return (o, lse) of a paged prefill (packed queries)."""
+    o = torch.empty_like(q)
+    lse = torch.empty((q.shape[1], q.shape[0]), dtype=torch.float32, device=q.device)
+    attn_fwd_paged(q, k_cache, v_cache, o, lse, qo_indptr, kv_indptr, kv_indices, max_qlen,
+                   causal, scale, **host)
+    return o, lse
+
+
+def decode_workspace_for(q, k_cache, max_kvlen: int) -> torch.Tensor:
+    batch, Hq, D = q.shape
+    n = attn_decode_paged_workspace_size(batch, max_kvlen, Hq, k_cache.shape[1], D)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=q.device)
+
+
+def decode_paged(q, k_cache, v_cache, kv_indptr, kv_indices, max_kvlen: int, scale: float,
+                 workspace=None, **host):
+    """Return (o, lse) of a paged decode step (one query per request)."""
+    o = torch.empty_like(q)
+    lse = torch.empty((q.shape[1], q.shape[0]), dtype=torch.float32, device=q.device)
+    ws = workspace if workspace is not None else decode_workspace_for(q, k_cache, max_kvlen)
+    attn_decode_paged(q, k_cache, v_cache, o, lse, kv_indptr, kv_indices, max_kvlen, scale, ws,
+                      **host)
+    return o, lse
 
 def forward(q, k, v, causal: bool, scale: float, cu_seqlens=None, max_seqlen: int = 0,
             cu_seqlens_host=None):

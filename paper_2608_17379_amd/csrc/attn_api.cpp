@@ -132,6 +132,22 @@ int bwd_common(const void* q, const void* k, const void* v, const void* o, const
   return attn::launch_bwd(a, D, phases, stream) == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
 }
 
+// A paged cache must be addressable with 31-bit byte offsets from the start
+// of any head's first row, and its page-index array with 31-bit offsets.
+int check_cache(int num_pages, int nnz, int Hkv, int D) {
+  if (num_pages < 0 || nnz < 0 || nnz > (1 << 29)) return ATTN_ERR_SHAPE;
+  if ((int64_t)num_pages * Hkv * D * 2 > 0x7fffffff) return ATTN_ERR_SHAPE;
+  return ATTN_OK;
+}
+
+bool misaligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) != 0; }
+
+int64_t decode_chunks(int max_kvlen) {
+  return ((int64_t)max_kvlen + attn::kDecodeChunk - 1) / attn::kDecodeChunk;
+}
+
+size_t round256(int64_t bytes) { return (size_t)((bytes + 255) / 256 * 256); }
+
 size_t delta_bytes(int64_t rows_times_heads) {
   // fp32 Delta and fp32 L log2(e) per (row, query head), each array rounded
   // up to 256 bytes.
@@ -233,15 +249,88 @@ int attn_bwd_varlen(const void* q, const void* k, const void* v, const void* o, 
                                 ATTN_BWD_DQ | ATTN_BWD_DKDV, stream);
 }
 
+int attn_fwd_paged(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse,
+                   const int* qo_indptr, const int* kv_indptr, const int* kv_indices, int batch,
+                   int max_qlen, int total_q, int nnz, int num_pages, int Hq, int Hkv, int D,
+                   int causal, float scale, hipStream_t stream) {
+  int st = check_common(Hq, Hkv, D, causal, scale);
+  if (st != ATTN_OK) return st;
+  if (batch < 0 || total_q < 0 || check_rows(max_qlen) != ATTN_OK) return ATTN_ERR_SHAPE;
+  if ((st = check_cache(num_pages, nnz, Hkv, D)) != ATTN_OK) return st;
+  if ((int64_t)batch * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
+  if (batch == 0 || total_q == 0) return ATTN_OK;
+  if (max_qlen < 1) return ATTN_ERR_VALUE;
+  if (!qo_indptr || !kv_indptr || (nnz > 0 && !kv_indices)) return ATTN_ERR_NULL;
+  if (misaligned4(qo_indptr) || misaligned4(kv_indptr) || misaligned4(kv_indices))
+    return ATTN_ERR_ALIGN;
+  Layout L = packed_layout(qo_indptr, batch, max_qlen, total_q, Hq, Hkv, D);
+  // The cache [num_pages, Hkv, D] has the packed key layout with a page per row.
+  L.kv_cu = kv_indptr;
+  L.kv_idx = kv_indices;
+  L.nnz = nnz;
+  L.num_pages = num_pages;
+  return fwd_common(q, k_cache, v_cache, o, lse, L, D, causal, scale, stream);
+}
+
+size_t attn_decode_paged_workspace_size(int batch, int max_kvlen, int Hq, int Hkv, int D) {
+  (void)Hkv;
+  if (batch <= 0 || max_kvlen <= 0 || Hq <= 0 || D <= 0) return 0;
+  const int64_t slots = (int64_t)batch * Hq * decode_chunks(max_kvlen);
+  return round256(slots * D * 4) + round256(slots * 4);
+}
+
+int attn_decode_paged(const void* q, const void* k_cache, const void* v_cache, void* o,
+                      float* lse, const int* kv_indptr, const int* kv_indices, int batch,
+                      int max_kvlen, int nnz, int num_pages, int Hq, int Hkv, int D, float scale,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  int st = check_common(Hq, Hkv, D, 0, scale);
+  if (st != ATTN_OK) return st;
+  if (Hq / Hkv > 32) return ATTN_ERR_GQA;
+  if (batch < 0 || check_rows(max_kvlen) != ATTN_OK) return ATTN_ERR_SHAPE;
+  if ((st = check_cache(num_pages, nnz, Hkv, D)) != ATTN_OK) return st;
+  if ((int64_t)batch * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
+  if (batch == 0) return ATTN_OK;
+  if (max_kvlen < 1) return ATTN_ERR_VALUE;
+  if (any_null({q, k_cache, v_cache, o, lse, kv_indptr}) || (nnz > 0 && !kv_indices))
+    return ATTN_ERR_NULL;
+  if (any_misaligned({q, k_cache, v_cache, o, lse})) return ATTN_ERR_ALIGN;
+  if (misaligned4(kv_indptr) || misaligned4(kv_indices)) return ATTN_ERR_ALIGN;
+  const size_t need = attn_decode_paged_workspace_size(batch, max_kvlen, Hq, Hkv, D);
+  if (!workspace || workspace_bytes < need) return ATTN_ERR_WORKSPACE;
+  if (misaligned(workspace)) return ATTN_ERR_ALIGN;
+  attn::DecodeArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k_cache);
+  a.v = static_cast<const uint16_t*>(v_cache);
+  a.o = static_cast<uint16_t*>(o);
+  a.lse = lse;
+  a.kv_cu = kv_indptr;
+  a.kv_idx = kv_indices;
+  a.batch = batch;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.group = Hq / Hkv;
+  a.nnz = nnz;
+  a.num_pages = num_pages;
+  a.max_kvlen = max_kvlen;
+  a.nchunk = (int)decode_chunks(max_kvlen);
+  a.scale_log2 = scale * 1.4426950408889634f;
+  const int64_t slots = (int64_t)batch * Hq * a.nchunk;
+  a.part_o = static_cast<float*>(workspace);
+  a.part_lse = reinterpret_cast<float*>(static_cast<char*>(workspace) + round256(slots * D * 4));
+  return attn::launch_decode(a, D, stream) == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
+}
+
 const char* attn_status_string(int status) {
   switch (status) {
     case ATTN_OK: return "ok";
     case ATTN_ERR_NULL: return "a required pointer is null";
     case ATTN_ERR_SHAPE: return "a size is negative, a head count is below 1, or a size is too large";
-    case ATTN_ERR_GQA: return "Hq is not a multiple of Hkv";
+    case ATTN_ERR_GQA:
+      return "Hq is not a multiple of Hkv, or (decode) Hq/Hkv is larger than 32";
     case ATTN_ERR_HEAD_DIM: return "head dimension must be 64, 96 or 128";
     case ATTN_ERR_ALIGN: return "a pointer is not 16-byte aligned";
-    case ATTN_ERR_WORKSPACE: return "workspace is null or smaller than attn_bwd_workspace_size()";
+    case ATTN_ERR_WORKSPACE: return "workspace is null or smaller than the size function returns";
     case ATTN_ERR_HIP: return "a kernel launch failed";
     case ATTN_ERR_VALUE:
       return "scale is not finite and > 0, causal is not 0 or 1, max_seqlen < 1, or a bad phase "

@@ -20,7 +20,10 @@
 //
 // K and V tiles go from global memory straight into a ring of LDS stages
 // (buffer_load ... lds, bounded at the sequence end so that rows past it read
-// as zero), issued a stage ahead, with one barrier per tile.  Both stay
+// as zero), issued a stage ahead, with one barrier per tile.  With a paged
+// cache (page size 1) each lane's copy offset comes from the page number of
+// its tile row, so the gather costs no extra pass; the page numbers are
+// fetched one tile ahead, and a page outside the cache reads as zeros.  Both stay
 // row-major in LDS: K is read as 16-byte rows, and the A operand V^T comes
 // out of the V tile through the transposing read ds_read_b64_tr_b16, so no
 // register staging or transposing store is needed.
@@ -40,7 +43,7 @@ constexpr float kRescaleSlack = 8.0f;   // log2 of the largest P entry allowed
 // separate objects so that the compiler can tell a stage being filled by DMA
 // from the one being read and does not wait for the prefetch.
 
-template <int D>
+template <int D, bool PAGED>
 __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   using Tile = AsyncTile<D>;
   constexpr int P = Tile::P;   // LDS row pitch (elements)
@@ -57,6 +60,12 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   const int z = blockIdx.x / L.Hq, h = blockIdx.x % L.Hq;
   const int hk = h / L.group;
   const Segment seg = segment_of(L, z);
+  // Keys: the segment's own rows, or (paged) its pages; the queries are the
+  // last seg.len of the kv_len key positions, so query row i sits at key
+  // position i + dpos.
+  const Segment kseg = PAGED ? kv_segment_of(L, z) : seg;
+  const int kv_len = kseg.len;
+  const int dpos = PAGED ? kv_len - seg.len : 0;
   // Query blocks nqt - 1 - p and p of the segment, in that order: under the
   // causal mask every workgroup then has the same number of key tiles, so the
   // two workgroups sharing a CU finish together.
@@ -74,8 +83,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
     const int q0 = qt * kBM;
     const int64_t qoff = (int64_t)seg.start * L.q_row + (int64_t)z * L.q_batch +
                          (int64_t)h * L.q_head;
-    const int64_t kvoff = (int64_t)seg.start * L.kv_row + (int64_t)z * L.kv_batch +
-                          (int64_t)hk * L.kv_head;
+    const int64_t kvoff = PAGED ? (int64_t)hk * L.kv_head
+                                : (int64_t)seg.start * L.kv_row + (int64_t)z * L.kv_batch +
+                                      (int64_t)hk * L.kv_head;
     const int64_t roff = (int64_t)seg.start + (int64_t)z * L.r_batch + (int64_t)h * L.r_head;
     const uint16_t* kp = a.k + kvoff;
     const uint16_t* vp = a.v + kvoff;
@@ -92,7 +102,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
       for (int c = 0; c < D / 16; ++c) qreg[c] = bload16(rq, base + 32 * c);
     }
 
-    const int kend = a.causal ? min(seg.len, q0 + kBM) : seg.len;
+    const int kend = a.causal ? min(kv_len, max(0, q0 + kBM + dpos)) : kv_len;
     const int nkt = (kend + kBN - 1) / kBN;
 
     const Tile dma(wave, lane, (int)(L.kv_row * 2));
@@ -110,8 +120,42 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
     // Fields used inside the lambdas below, as plain values (capturing the
     // kernel argument itself can make the compiler spill it to scratch).
     const bool causal = a.causal != 0;
-    const int len = seg.len;
     const int64_t kv_row = L.kv_row;
+
+    // Paged keys: tile rows are gathered through the page indices, which are
+    // fetched one tile ahead of the copies that use them.
+    int pidx[Tile::NJ];
+    const int num_pages = L.num_pages;
+    const int cache_row_bytes = (int)(L.kv_row * 2);
+    const int64_t cache_bytes = PAGED ? (int64_t)L.num_pages * L.kv_row * 2 - kvoff * 2 : 0;
+    const rsrc_t kcache = make_rsrc(kp, cache_bytes);
+    const rsrc_t vcache = make_rsrc(vp, cache_bytes);
+    const rsrc_t ixr = make_rsrc(PAGED ? L.kv_idx + kseg.start : nullptr,
+                                 PAGED ? (int64_t)kv_len * 4 : 0);
+    auto fetch = [&](int kt) __attribute__((always_inline)) {
+#pragma unroll
+      for (int j = 0; j < Tile::NJ; ++j)
+        pidx[j] = bload4(ixr, 4 * (kt * kBN + Tile::row_of(wave, j, lane)));
+    };
+    // Start the copies of tile kt into stages kd, vd (and, paged, the index
+    // fetch of tile kt + 1).
+    auto load_tile = [&](int kt, uint16_t* kd, uint16_t* vd) __attribute__((always_inline)) {
+      if constexpr (PAGED) {
+        int off[Tile::NJ];
+#pragma unroll
+        for (int j = 0; j < Tile::NJ; ++j) {
+          const int key = kt * kBN + Tile::row_of(wave, j, lane);
+          off[j] = Tile::gather_off(wave, j, lane, pidx[j], key < kv_len, num_pages,
+                                    cache_row_bytes);
+        }
+        dma.load_at(kcache, off, kd, wave);
+        dma.load_at(vcache, off, vd, wave);
+        if (kt + 1 < nkt) fetch(kt + 1);
+      } else {
+        dma.load(rows_rsrc(kp, kt * kBN, kv_len, kv_row), kd, wave);
+        dma.load(rows_rsrc(vp, kt * kBN, kv_len, kv_row), vd, wave);
+      }
+    };
 
     auto compute = [&](int kt, const uint16_t* kt_lds, const uint16_t* vt_lds) __attribute__((always_inline)) {
       const int k0 = kt * kBN;
@@ -127,13 +171,13 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
           s[kb] = mfma32(ld16(kt_lds + kr.rm[c] + 32 * kb * P), qreg[c], s[kb]);
 
       // s[kb][r] is the raw score of key k0 + 32kb + 8(r/4) + 4half + r%4.
-      if ((a.causal && k0 + kBN - 1 > qw0) || k0 + kBN > seg.len) {
+      if ((a.causal && k0 + kBN - 1 > qw0 + dpos) || k0 + kBN > kv_len) {
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int key = k0 + 32 * kb + 8 * (r / 4) + 4 * half + (r % 4);
-            const bool masked = (a.causal && key > qrow) || key >= seg.len;
+            const bool masked = (a.causal && key > qrow + dpos) || key >= kv_len;
             s[kb][r] = masked ? -INFINITY : s[kb][r];
           }
       }
@@ -146,7 +190,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
       const float mt = mx * sl2;   // this tile's row max in exp2 units
       if (__ballot(mt > mref + kRescaleSlack)) {
         const float mnew = fmaxf(mref, mt);
-        const float alpha = fast_exp2(mref - mnew);   // 0 on the first visible tile
+        // 0 on the first visible tile; 1 for a row that has seen no key yet
+        // (both maxima -inf), whose O and l are still 0.
+        const float alpha = mnew == -INFINITY ? 1.f : fast_exp2(mref - mnew);
         lsum *= alpha;
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
@@ -186,19 +232,17 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
                     uint16_t* vn) __attribute__((always_inline)) {
       wait_vm<0>();
       __syncthreads();
-      if (kt + 1 < nkt) {
-        dma.load(rows_rsrc(kp, (kt + 1) * kBN, len, kv_row), kn, wave);
-        dma.load(rows_rsrc(vp, (kt + 1) * kBN, len, kv_row), vn, wave);
-      }
+      if (kt + 1 < nkt) load_tile(kt + 1, kn, vn);
       if (work) compute(kt, kc, vc);
     };
 
     // Tiles past this wavefront's last query are fully masked for it: the
     // wavefront only joins their barriers and loads.
-    const int nkt_w = causal ? min(nkt, (qw0 + 31) / kBN + 1) : nkt;
+    const int last_key = qw0 + 31 + dpos;   // the wavefront's last visible key (causal)
+    const int nkt_w = causal ? (last_key < 0 ? 0 : min(nkt, last_key / kBN + 1)) : nkt;
     if (nkt > 0) {
-      dma.load(rows_rsrc(kp, 0, seg.len, L.kv_row), sk0, wave);
-      dma.load(rows_rsrc(vp, 0, seg.len, L.kv_row), sv0, wave);
+      if constexpr (PAGED) fetch(0);
+      load_tile(0, sk0, sv0);
     }
     wait_vm<0>();   // Q rows and the first tile
     int kt = 0;
@@ -238,9 +282,22 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
 
 // Explicit instantiations: without them the host compiler may skip the
 // launch stubs of these templates (leaving undefined symbols in the library).
-template __global__ void fwd_kernel<64>(FwdArgs);
-template __global__ void fwd_kernel<96>(FwdArgs);
-template __global__ void fwd_kernel<128>(FwdArgs);
+template __global__ void fwd_kernel<64, false>(FwdArgs);
+template __global__ void fwd_kernel<96, false>(FwdArgs);
+template __global__ void fwd_kernel<128, false>(FwdArgs);
+template __global__ void fwd_kernel<64, true>(FwdArgs);
+template __global__ void fwd_kernel<96, true>(FwdArgs);
+template __global__ void fwd_kernel<128, true>(FwdArgs);
+
+template <bool PAGED>
+void launch_fwd_p(const FwdArgs& a, int D, dim3 grid, hipStream_t stream) {
+  if (D == 64)
+    hipLaunchKernelGGL((fwd_kernel<64, PAGED>), grid, dim3(kThreads), 0, stream, a);
+  else if (D == 96)
+    hipLaunchKernelGGL((fwd_kernel<96, PAGED>), grid, dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((fwd_kernel<128, PAGED>), grid, dim3(kThreads), 0, stream, a);
+}
 
 }  // namespace
 
@@ -248,12 +305,10 @@ hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream) {
   // Each workgroup takes a query block and its mirror (see the kernel).
   const int nqt = (a.L.S + kBM - 1) / kBM;
   const dim3 grid((unsigned)(a.L.nseg * a.L.Hq), (unsigned)((nqt + 1) / 2));
-  if (D == 64)
-    hipLaunchKernelGGL(fwd_kernel<64>, grid, dim3(kThreads), 0, stream, a);
-  else if (D == 96)
-    hipLaunchKernelGGL(fwd_kernel<96>, grid, dim3(kThreads), 0, stream, a);
+  if (a.L.kv_cu)
+    launch_fwd_p<true>(a, D, grid, stream);
   else
-    hipLaunchKernelGGL(fwd_kernel<128>, grid, dim3(kThreads), 0, stream, a);
+    launch_fwd_p<false>(a, D, grid, stream);
   return hipGetLastError();
 }
 

@@ -25,6 +25,15 @@ struct Layout {
   int64_t q_batch, q_head, q_row;     // strides of q-like tensors
   int64_t kv_batch, kv_head, kv_row;  // strides of k-like tensors
   int64_t r_batch, r_head;            // strides of lse / Delta (row stride 1)
+  // Paged key/value cache (page size 1), forward only; kv_cu == nullptr
+  // otherwise.  Keys of segment z are the cache rows kv_idx[kv_cu[z]] ..
+  // kv_idx[kv_cu[z+1]-1], each kv_row elements apart (k-like strides with
+  // kv_batch = 0 and start 0); the segment's queries are the last of its
+  // key positions.
+  const int* kv_cu;        // [nseg + 1] offsets into kv_idx (device)
+  const int* kv_idx;       // [nnz] page numbers (device)
+  int nnz;                 // entries of kv_idx
+  int num_pages;           // rows of the cache
 };
 
 struct FwdArgs {
@@ -56,8 +65,29 @@ struct BwdArgs {
   int causal;
 };
 
+// Paged decode: one query row per request (q, o [batch, Hq, D], lse
+// [Hq, batch]) against its pages, split into chunks of keys whose partial
+// results go to the workspace and are merged by a second kernel.
+struct DecodeArgs {
+  const uint16_t* q;
+  const uint16_t* k;       // cache [num_pages, Hkv, D]
+  const uint16_t* v;
+  uint16_t* o;
+  float* lse;
+  const int* kv_cu;        // [batch + 1]
+  const int* kv_idx;       // [nnz]
+  int batch, Hq, Hkv, group, nnz, num_pages, max_kvlen;
+  int nchunk;              // key chunks per request (max_kvlen rounded up)
+  float scale_log2;        // softmax scale * log2(e)
+  float* part_o;           // workspace [batch, Hq, nchunk, D] fp32
+  float* part_lse;         // workspace [batch, Hq, nchunk] fp32, log2 units
+};
+
 // Launchers: enqueue on `stream`, return the hipGetLastError() of the launch.
 hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream);
+// Keys per chunk of the decode split (sizes the workspace).
+constexpr int kDecodeChunk = 128;
+hipError_t launch_decode(const DecodeArgs& a, int D, hipStream_t stream);
 // phases: bit 0 = Delta and dQ kernel, bit 1 = dK/dV kernel.
 hipError_t launch_bwd(const BwdArgs& a, int D, int phases, hipStream_t stream);
 

@@ -153,12 +153,40 @@ struct AsyncTile {
   // Enqueue this wavefront's share of a tile: rows [0, 64) of `src` into
   // `dst` (the tile base in LDS).
   __device__ __forceinline__ void load(rsrc_t src, uint16_t* dst, int wave) const {
+    load_at(src, goff, dst, wave);
+  }
+  // The same with explicit per-lane source offsets (gathered rows).
+  __device__ __forceinline__ void load_at(rsrc_t src, const int (&off)[NJ], uint16_t* dst,
+                                          int wave) const {
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          src, (ATTN_LDS void*)(dst + (wave * NJ + j) * 64 * 8), 16, goff[j], 0, 0, 0);
+          src, (ATTN_LDS void*)(dst + (wave * NJ + j) * 64 * 8), 16, off[j], 0, 0, 0);
+  }
+  // Tile row and logical 16-byte chunk that this lane copies in DMA
+  // instruction j.
+  static __device__ __forceinline__ int row_of(int wave, int j, int lane) {
+    return ((wave * NJ + j) * 64 + lane) / CPR;
+  }
+  static __device__ __forceinline__ int chunk_of(int wave, int j, int lane) {
+    const int p = (wave * NJ + j) * 64 + lane;
+    return (p % CPR) ^ tile_swz<P>(p / CPR);
+  }
+  // Source offset of instruction j when the tile's rows are gathered: row r
+  // of the tile is row page[r] of a cache whose rows are row_bytes apart.
+  // Invalid rows (ok false, or page outside [0, num_pages)) and pad chunks
+  // read zeros.
+  static __device__ __forceinline__ int gather_off(int wave, int j, int lane, int page, bool ok,
+                                                   int num_pages, int row_bytes) {
+    const int c = chunk_of(wave, j, lane);
+    ok = ok && (unsigned)page < (unsigned)num_pages && c < D / 8;
+    return ok ? page * row_bytes + 16 * c : kPadOffset;
   }
 };
+
+__device__ __forceinline__ int bload4(rsrc_t r, int byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0);
+}
 
 // Row-major read offsets (elements) of an MFMA operand over rows
 // 32*b + (lane % 32), 16-byte chunk 2c + half: rm[c] + 32*b*P.
@@ -284,6 +312,16 @@ struct Segment {
   int start;   // first row (packed) or 0
   int len;     // rows in this segment
 };
+
+// Keys of segment z of a paged layout: offsets into the page-index array,
+// clamped into [0, nnz].
+template <typename LayoutT>
+__device__ __forceinline__ Segment kv_segment_of(const LayoutT& L, int z) {
+  int a = L.kv_cu[z], b = L.kv_cu[z + 1];
+  a = a < 0 ? 0 : (a > L.nnz ? L.nnz : a);
+  b = b < a ? a : (b > L.nnz ? L.nnz : b);
+  return Segment{a, b - a};
+}
 
 template <typename LayoutT>
 __device__ __forceinline__ Segment segment_of(const LayoutT& L, int z) {

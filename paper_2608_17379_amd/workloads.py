@@ -146,6 +146,82 @@ def make_inputs(w: Workload, seed: int = 0, lengths: Optional[List[int]] = None)
     return Inputs(w, q, k, v, do, cu)
 
 
+# ---------------------------------------------------------------------------
+# Paged key/value cache (page size 1): the paper's paged causal prefill and
+# paged decode workloads give head counts, the request count, the number of
+# page indices and the cache size; the lengths and the pages are drawn here.
+# ---------------------------------------------------------------------------
+
+@dataclass(frozen=True)
+class PagedWorkload:
+    name: str
+    batch: int        # requests
+    Hq: int
+    Hkv: int
+    D: int
+    nnz: int          # page indices over all requests (total keys)
+    num_pages: int    # pages in the cache
+    decode: bool      # one query per request (else as many queries as keys)
+    causal: bool = True
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / math.sqrt(self.D)
+
+
+PAGED_WORKLOADS = {
+    "paged_prefill_causal_q892_p43676_hq24_hkv8_d128": PagedWorkload(
+        "paged_prefill_causal_q892_p43676_hq24_hkv8_d128", 1, 24, 8, 128, 892, 43676, False),
+    "paged_decode_b15_nnz9625_p42784_hq24_hkv8_d128": PagedWorkload(
+        "paged_decode_b15_nnz9625_p42784_hq24_hkv8_d128", 15, 24, 8, 128, 9625, 42784, True),
+}
+
+
+@dataclass
+class PagedInputs:
+    workload: PagedWorkload
+    q: torch.Tensor            # [Tq, Hq, D] (decode: [batch, Hq, D])
+    k_cache: torch.Tensor      # [num_pages, Hkv, D]
+    v_cache: torch.Tensor
+    qo_indptr: List[int]
+    kv_indptr: List[int]
+    kv_indices: List[int]
+
+    @property
+    def max_qlen(self) -> int:
+        return max(b - a for a, b in zip(self.qo_indptr, self.qo_indptr[1:]))
+
+    @property
+    def max_kvlen(self) -> int:
+        return max(b - a for a, b in zip(self.kv_indptr, self.kv_indptr[1:]))
+
+
+def make_paged_inputs(w: PagedWorkload, seed: int = 0,
+                      kv_lens: Optional[List[int]] = None) -> PagedInputs:
+    """Draw, in order: the key count of each request (a random composition of
+    nnz), the page of every key (distinct pages, a uniformly random subset of
+    the cache in random order), then Q, the K cache and the V cache, i.i.d.
+    N(0, 1) rounded to bf16.  ``kv_lens`` overrides the drawn counts (their
+    sum must then be nnz)."""
+    gen = torch.Generator().manual_seed(seed)
+    if kv_lens is None:
+        kv_lens = random_composition(gen, w.nnz, w.batch) if w.nnz >= w.batch else None
+    if kv_lens is None or sum(kv_lens) != w.nnz or len(kv_lens) != w.batch:
+        raise ValueError("kv_lens must be batch counts summing to nnz")
+    if w.nnz > w.num_pages:
+        raise ValueError("more keys than pages")
+    pages = torch.randperm(w.num_pages, generator=gen)[:w.nnz].tolist()
+    q_lens = [1] * w.batch if w.decode else list(kv_lens)
+    qo, kv = [0], [0]
+    for a, b in zip(q_lens, kv_lens):
+        qo.append(qo[-1] + a)
+        kv.append(kv[-1] + b)
+    q = _randn_bf16(gen, (qo[-1], w.Hq, w.D))
+    kc = _randn_bf16(gen, (w.num_pages, w.Hkv, w.D))
+    vc = _randn_bf16(gen, (w.num_pages, w.Hkv, w.D))
+    return PagedInputs(w, q, kc, vc, qo, kv, pages)
+
+
 def small(name: str, B: int, Hq: int, Hkv: int, S: int, D: int, causal: bool,
           varlen: bool = False, qk_mult: float = 1.0) -> Workload:
     """An ad-hoc workload for shape sweeps (same drawing recipe)."""

@@ -145,3 +145,67 @@ def test_cu_seqlens_host_check():
     for bad, total, ms in (([1, 3], 3, 5), ([0, 4, 3], 3, 5), ([0, 3], 4, 5), ([0, 9], 9, 5)):
         with pytest.raises(ValueError):
             attn.check_cu_seqlens(bad, total, ms)
+
+
+def fwdp(**kw):
+    args = dict(q=A, k=A, v=A, o=A, lse=A, qo=A, kv=A, idx=A, batch=2, mq=64, Tq=100, nnz=120,
+                P=1000, Hq=4, Hkv=2, D=128, causal=1, scale=0.1)
+    args.update(kw)
+    return attn.lib().attn_fwd_paged(*(args[n] for n in (
+        "q", "k", "v", "o", "lse", "qo", "kv", "idx", "batch", "mq", "Tq", "nnz", "P", "Hq", "Hkv",
+        "D", "causal", "scale")), None)
+
+
+def dec(**kw):
+    args = dict(q=A, k=A, v=A, o=A, lse=A, kv=A, idx=A, batch=3, mk=500, nnz=900, P=1000, Hq=24,
+                Hkv=8, D=128, scale=0.1, ws=A, wsb=1 << 24)
+    args.update(kw)
+    return attn.lib().attn_decode_paged(*(args[n] for n in (
+        "q", "k", "v", "o", "lse", "kv", "idx", "batch", "mk", "nnz", "P", "Hq", "Hkv", "D",
+        "scale", "ws", "wsb")), None)
+
+
+@pytest.mark.parametrize("call", [fwdp, dec])
+def test_paged_validation(call):
+    assert call(Hq=3, Hkv=2) == -3
+    assert call(D=80) == -4
+    assert call(scale=0.0) == -8
+    assert call(batch=-1) == -2
+    assert call(nnz=-1) == -2
+    assert call(nnz=(1 << 29) + 1) == -2
+    assert call(P=-1) == -2
+    assert call(P=(1 << 31) // (2 * 128 * 2) + 1) == -2   # cache bytes beyond 2^31
+    assert call(kv=0) == -1
+    assert call(idx=0) == -1
+    assert call(kv=A + 2) == -5
+    assert call(idx=A + 1) == -5
+    assert call(q=A + 8) == -5
+    assert call(batch=0, q=0, kv=0, idx=0) == 0
+
+
+def test_paged_prefill_specific_validation():
+    assert fwdp(causal=2) == -8
+    assert fwdp(mq=0) == -8
+    assert fwdp(qo=0) == -1
+    assert fwdp(Tq=-1) == -2
+    assert fwdp(Tq=0, q=0, qo=0) == 0
+
+
+def test_decode_specific_validation():
+    assert dec(Hq=66, Hkv=2) == -3     # more than 32 query heads per kv head
+    assert dec(mk=0) == -8
+    need = attn.attn_decode_paged_workspace_size(3, 500, 24, 8, 128)
+    assert need >= 3 * 24 * 4 * 129 * 4 and need % 256 == 0
+    assert dec(wsb=need - 1) == -6
+    assert dec(ws=0) == -6
+    assert dec(ws=A + 8) == -5
+    assert attn.attn_decode_paged_workspace_size(0, 500, 24, 8, 128) == 0
+
+
+def test_paged_host_check():
+    attn.check_paged_host([0, 2, 2, 5], [4, 1, 0, 2, 3], 5, 3)
+    for kv, idx, p, mk in (([1, 2], [0, 1], 5, None), ([0, 2, 1], [0, 1], 5, None),
+                           ([0, 2], [0, 5], 5, None), ([0, 2], [0, -1], 5, None),
+                           ([0, 3], [0, 1, 2], 5, 2), ([0, 2], [0, 1, 2], 5, None)):
+        with pytest.raises(ValueError):
+            attn.check_paged_host(kv, idx, p, mk)

@@ -3,11 +3,19 @@
 
     python bench.py [--steps K] [--warmup W] [--workload NAME]
 
+Without --workload it measures the headline workload (B4 H16 S2048 D128
+causal).  The paged-cache workloads (paged prefill, paged decode) are forward
+only, as in the paper: their step is one attn_fwd_paged call (TFLOP/s) or one
+attn_decode_paged call (its split and merge kernels; HBM GB/s, with the
+roofline against 8 TB/s since decode reads each key and value once).
+
 A step is one forward (attn_fwd) and one backward (attn_bwd_phases with the
 Delta/dQ phase, then the dK/dV phase: together exactly attn_bwd) over one
 batch of seeded synthetic bf16 inputs already resident in HBM.  W untimed
 steps, then K timed steps between two synchronisations; one JSON line is
-printed.
+printed.  Before the timed steps the GPU runs a spin kernel long enough for
+the host to enqueue all K steps, so the steps run back to back and the
+timing is the GPU's, not the host's launch rate.
 
 FLOP convention: forward 4*B*Hq*S^2*D (halved when causal; packed input sums
 L^2 over sequences), backward 2.5x forward.  TFLOP/s = (forward + backward
@@ -44,11 +52,13 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6
+PEAK_HBM_GBS = 8000.0
 METRIC = "attention fwd/bwd TFLOP/s + % bf16 MFMA peak, B4 H16 S2048 D128 causal"
 KERNELS = ("fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel")
 GEMMS = {"fwd_kernel": 2, "bwd_dq_kernel": 3, "bwd_dkdv_kernel": 4}
 KERNEL_SOURCES = {"fwd_kernel": "attn_fwd.hip", "bwd_dq_kernel": "attn_bwd.hip",
-                  "bwd_dkdv_kernel": "attn_bwd.hip"}
+                  "bwd_dkdv_kernel": "attn_bwd.hip", "decode_split_kernel": "attn_decode.hip",
+                  "decode_merge_kernel": "attn_decode.hip"}
 
 
 def fwd_flops(w, cu_seqlens=None) -> float:
@@ -126,6 +136,171 @@ def cpu_baseline(w, x, seconds: float):
     }
 
 
+def hold_gpu_for_enqueue(host_ms_per_step: float, steps: int) -> None:
+    """Occupy the GPU with torch's spin kernel for longer than the host needs
+    to enqueue `steps` steps, so that the timed steps then run back to back:
+    the HIP events between launches measure the kernels, not the host's
+    launch rate (which matters for microsecond-scale kernels)."""
+    import torch
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    torch.cuda._sleep(1_000_000)
+    b.record()
+    torch.cuda.synchronize()
+    cycles_per_ms = 1_000_000 / max(a.elapsed_time(b), 1e-3)
+    want_ms = min(2000.0, 1.0 + 1.5 * host_ms_per_step * steps)
+    torch.cuda._sleep(int(cycles_per_ms * want_ms))
+
+
+# ---------------------------------------------------------------------------
+# Paged key/value cache workloads (forward only, as in the paper)
+# ---------------------------------------------------------------------------
+
+def paged_flops(x) -> float:
+    """4 * Hq * D * sum(q_len * kv_len), halved when causal with q_len ==
+    kv_len (the same convention as the fixed-length forward)."""
+    w = x.workload
+    tot = 0.0
+    for (qa, qb), (ka, kb) in zip(zip(x.qo_indptr, x.qo_indptr[1:]),
+                                  zip(x.kv_indptr, x.kv_indptr[1:])):
+        ql, kl = qb - qa, kb - ka
+        tot += ql * kl * (0.5 if w.causal and ql == kl and ql > 1 else 1.0)
+    return 4.0 * w.Hq * w.D * tot
+
+
+def decode_bytes(x) -> dict:
+    """Algorithmic HBM bytes of one decode step, by kernel: the split kernel
+    reads every key and value row of every request once, the queries and the
+    page indices; the outputs (bf16 O, fp32 LSE) are counted for the merge."""
+    w = x.workload
+    nnz, batch = len(x.kv_indices), w.batch
+    kv = 2 * nnz * w.Hkv * w.D * 2
+    q = batch * w.Hq * w.D * 2
+    idx = 4 * (nnz + batch + 1)
+    out = batch * w.Hq * (w.D * 2 + 4)
+    return {"decode_split_kernel": kv + q + idx, "decode_merge_kernel": out}
+
+
+def cpu_baseline_paged(x, seconds: float, unit_of):
+    """Oracle (fp64, CPU) on the whole paged workload, repeated until about
+    `seconds` have elapsed; `unit_of(passes, dt)` turns it into the metric."""
+    import torch
+    import oracle
+    w = x.workload
+    t0, passes = time.perf_counter(), 0
+    while passes == 0 or time.perf_counter() - t0 < seconds:
+        oracle.attention_forward_paged(x.q, x.k_cache, x.v_cache, x.qo_indptr, x.kv_indptr,
+                                       x.kv_indices, w.causal, w.scale)
+        passes += 1
+    dt = time.perf_counter() - t0
+    value, unit = unit_of(passes, dt)
+    return {"value": round(value, 6), "unit": unit, "cores": torch.get_num_threads(),
+            "kind": "oracle",
+            "sample": f"the whole workload {w.name}, {passes} pass(es), fp64 forward, {dt:.1f} s"}
+
+
+def run_paged(args, w) -> int:
+    import torch
+    from paper_2608_17379_amd import attn
+    from paper_2608_17379_amd import workloads as wl
+
+    x = wl.make_paged_inputs(w, 0)
+    dev = torch.device("cuda", 0)
+    q, kc, vc = (t.to(dev) for t in (x.q, x.k_cache, x.v_cache))
+    qo = torch.tensor(x.qo_indptr, dtype=torch.int32, device=dev)
+    kv = torch.tensor(x.kv_indptr, dtype=torch.int32, device=dev)
+    idx = torch.tensor(x.kv_indices, dtype=torch.int32, device=dev)
+    o = torch.empty_like(q)
+    lse = torch.empty(w.Hq, q.shape[0], dtype=torch.float32, device=dev)
+    # The index arrays are checked once here; the timed calls skip the
+    # binding's host-side checks (they would otherwise dominate the step).
+    attn.check_cu_seqlens(x.qo_indptr, q.shape[0], x.max_qlen)
+    attn.check_paged_host(x.kv_indptr, x.kv_indices, w.num_pages, x.max_kvlen)
+    host = dict(checked=True)
+    if w.decode:
+        kernels = ("decode_split_kernel", "decode_merge_kernel")
+        ws = attn.decode_workspace_for(q, kc, x.max_kvlen)
+
+        def launch(i):
+            ph = (attn.ATTN_DECODE_SPLIT, attn.ATTN_DECODE_MERGE)[i]
+            attn.attn_decode_paged_phases(q, kc, vc, o, lse, kv, idx, x.max_kvlen, w.scale, ws,
+                                          ph, **host)
+    else:
+        kernels = ("fwd_kernel",)
+
+        def launch(i):
+            attn.attn_fwd_paged(q, kc, vc, o, lse, qo, kv, idx, x.max_qlen, w.causal, w.scale,
+                                **host)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        for i in range(len(kernels)):
+            launch(i)
+            if ev is not None:
+                ev[1 + i].record()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(kernels) + 1)]
+           for _ in range(max(args.steps, args.warmup))]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.warmup):
+        step(evs[i])
+    host_ms = (time.perf_counter() - t0) * 1e3 / max(1, args.warmup)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    hold_gpu_for_enqueue(host_ms, args.steps)
+    start.record()
+    for i in range(args.steps):
+        step(evs[i])
+    end.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(end) / args.steps
+    kern_ms = {n: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps
+               for j, n in enumerate(kernels)}
+    if not (torch.isfinite(o.float()).all() and torch.isfinite(lse).all()):
+        print("non-finite output", file=sys.stderr)
+        return 1
+
+    F = paged_flops(x)
+    cfg = {"workload": w.name, "batch": w.batch, "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D,
+           "nnz": w.nnz, "num_pages": w.num_pages, "page_size": 1, "causal": w.causal,
+           "decode": w.decode, "seed": 0,
+           "kv_lens": [b - a for a, b in zip(x.kv_indptr, x.kv_indptr[1:])]}
+    rec = {"n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (seeded i.i.d. N(0,1) bf16; seeded lengths and pages)",
+           "config": cfg, "kernel_ms": {n: round(t, 5) for n, t in kern_ms.items()}}
+    if w.decode:
+        by = decode_bytes(x)
+        total = sum(by.values())
+        dom = max(kernels, key=lambda n: kern_ms[n])
+        ach = by[dom] / (kern_ms[dom] * 1e-3) / 1e9
+        rec.update({"metric": f"paged decode HBM GB/s, {w.name}",
+                    "value": round(total / (ms_step * 1e-3) / 1e9, 2), "unit": "GB/s",
+                    "tflops": round(F / (ms_step * 1e-3) / 1e12, 4),
+                    "roofline": {"kernel": dom, "bound": "hbm", "achieved": round(ach, 2),
+                                 "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                                 "frac": round(ach / PEAK_HBM_GBS, 4),
+                                 "traffic": load_traffic(dom, w.name)}})
+        unit_of = lambda n, dt: (total * n / dt / 1e9, "GB/s")
+    else:
+        ach = F / (kern_ms["fwd_kernel"] * 1e-3) / 1e12
+        rec.update({"metric": f"attention fwd TFLOP/s, {w.name}",
+                    "value": round(F / (ms_step * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
+                    "pct_peak": round(100 * F / (ms_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+                    "roofline": {"kernel": "fwd_kernel", "bound": "mfma", "achieved": round(ach, 2),
+                                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                                 "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                                 "traffic": load_traffic("fwd_kernel", w.name)}})
+        unit_of = lambda n, dt: (F * n / dt / 1e12, "TFLOP/s")
+    rec["cpu_baseline"] = None if args.no_cpu_baseline else \
+        cpu_baseline_paged(x, args.cpu_seconds, unit_of)
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
 def copy_calibration(nbytes: int, reps: int) -> None:
     """A plain device copy of known size, for scaling HBM byte counters."""
     import torch
@@ -164,7 +339,14 @@ def main(argv=None) -> int:
         copy_calibration(args.copy_calibration, max(1, args.steps))
         return 0
 
-    w = wl.WORKLOADS[args.workload or wl.HEADLINE]
+    name = args.workload or wl.HEADLINE
+    if name in wl.PAGED_WORKLOADS:
+        return run_paged(args, wl.PAGED_WORKLOADS[name])
+    if name not in wl.WORKLOADS:
+        print(f"unknown workload {name}; known: "
+              + ", ".join(list(wl.WORKLOADS) + list(wl.PAGED_WORKLOADS)), file=sys.stderr)
+        return 2
+    w = wl.WORKLOADS[name]
     x = wl.make_inputs(w, 0)
     dev = torch.device("cuda", 0)
     q, k, v, do = (t.to(dev) for t in (x.q, x.k, x.v, x.do))
@@ -197,13 +379,15 @@ def main(argv=None) -> int:
             if ev is not None:
                 ev[2 + i].record()
 
-    for _ in range(args.warmup):
-        step()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)]
+           for _ in range(max(args.steps, args.warmup))]
     torch.cuda.synchronize()
-
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.warmup):
+        step(evs[i])
+    host_ms = (time.perf_counter() - t0) * 1e3 / max(1, args.warmup)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
+    hold_gpu_for_enqueue(host_ms, args.steps)
     start.record()
     for i in range(args.steps):
         step(evs[i])

@@ -186,7 +186,7 @@ int attn_fwd_paged(const void* q, const void* k_cache, const void* v_cache, void
                    hipStream_t stream);
 
 /* Bytes of workspace for attn_decode_paged (partial outputs of the key
- * chunks: fp32 [batch, Hq, ceil(max_kvlen / 128), D + 1], rounded up). */
+ * chunks: fp32 [batch, Hq, ceil(max_kvlen / 64), D + 1], rounded up). */
 size_t attn_decode_paged_workspace_size(int batch, int max_kvlen, int Hq, int Hkv, int D);
 
 /*
@@ -204,6 +204,26 @@ int attn_decode_paged(const void* q, const void* k_cache, const void* v_cache, v
                       int max_kvlen, int nnz, int num_pages, int Hq, int Hkv, int D,
                       float scale, void* workspace, size_t workspace_bytes,
                       hipStream_t stream);
+
+/*
+ * The decode in separately enqueued phases, for callers that time or
+ * schedule its two kernels on their own.  `phases` is a bit mask:
+ *   ATTN_DECODE_SPLIT  per-chunk partial results (and the final result of
+ *                      requests with at most 64 keys);
+ *   ATTN_DECODE_MERGE  the merge of the chunks of every longer request (and
+ *                      the result of requests with no keys), reading the
+ *                      workspace of an ATTN_DECODE_SPLIT phase enqueued
+ *                      earlier on the same stream with the same arguments.
+ * Both bits together are exactly attn_decode_paged; any other value returns
+ * ATTN_ERR_VALUE.
+ */
+#define ATTN_DECODE_SPLIT 1
+#define ATTN_DECODE_MERGE 2
+int attn_decode_paged_phases(const void* q, const void* k_cache, const void* v_cache, void* o,
+                             float* lse, const int* kv_indptr, const int* kv_indices,
+                             int batch, int max_kvlen, int nnz, int num_pages, int Hq,
+                             int Hkv, int D, float scale, void* workspace,
+                             size_t workspace_bytes, int phases, hipStream_t stream);
 
 /* Static, human-readable text for a status code (never null). */
 const char* attn_status_string(int status);

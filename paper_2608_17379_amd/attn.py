@@ -26,9 +26,11 @@ STATUS_NAMES = {
 EXPORTS = ("attn_fwd", "attn_bwd", "attn_bwd_workspace_size", "attn_fwd_varlen",
            "attn_bwd_varlen", "attn_bwd_varlen_workspace_size", "attn_bwd_phases",
            "attn_bwd_varlen_phases", "attn_fwd_paged", "attn_decode_paged_workspace_size",
-           "attn_decode_paged", "attn_status_string")
+           "attn_decode_paged", "attn_decode_paged_phases", "attn_status_string")
 ATTN_BWD_DQ = 1
 ATTN_BWD_DKDV = 2
+ATTN_DECODE_SPLIT = 1
+ATTN_DECODE_MERGE = 2
 
 
 class AttnError(RuntimeError):
@@ -70,6 +72,8 @@ def lib() -> ctypes.CDLL:
         l.attn_decode_paged_workspace_size.restype = _Z
         l.attn_decode_paged.argtypes = [_P] * 7 + [_I] * 7 + [_F, _P, _Z, _P]
         l.attn_decode_paged.restype = _I
+        l.attn_decode_paged_phases.argtypes = [_P] * 7 + [_I] * 7 + [_F, _P, _Z, _I, _P]
+        l.attn_decode_paged_phases.restype = _I
         l.attn_status_string.argtypes = [_I]
         l.attn_status_string.restype = ctypes.c_char_p
         _lib = l
@@ -264,7 +268,12 @@ def check_paged_host(kv_host: Sequence[int], idx_host: Sequence[int], num_pages:
 
 def attn_fwd_paged(q, k_cache, v_cache, o, lse, qo_indptr, kv_indptr, kv_indices,
                    max_qlen: int, causal: bool, scale: float, stream=None,
-                   qo_indptr_host=None, kv_indptr_host=None, kv_indices_host=None) -> None:
+                   qo_indptr_host=None, kv_indptr_host=None, kv_indices_host=None,
+                   checked: bool = False) -> None:
+    """Paged prefill.  The index arrays are checked on the host (from the
+    *_host copies when given, else from a device-to-host copy) unless
+    `checked` says the caller has already done so with check_cu_seqlens and
+    check_paged_host for these arrays."""
     Tq, Hq, D = q.shape
     P, Hkv = k_cache.shape[0], k_cache.shape[1]
     _shape(k_cache, (P, Hkv, D), "k_cache")
@@ -274,9 +283,10 @@ def attn_fwd_paged(q, k_cache, v_cache, o, lse, qo_indptr, kv_indptr, kv_indices
     batch = qo_indptr.numel() - 1
     if kv_indptr.numel() != batch + 1:
         raise ValueError("qo_indptr and kv_indptr must have the same length")
-    check_cu_seqlens(_host_list(qo_indptr, qo_indptr_host), Tq, max_qlen)
-    check_paged_host(_host_list(kv_indptr, kv_indptr_host),
-                     _host_list(kv_indices, kv_indices_host), P)
+    if not checked:
+        check_cu_seqlens(_host_list(qo_indptr, qo_indptr_host), Tq, max_qlen)
+        check_paged_host(_host_list(kv_indptr, kv_indptr_host),
+                         _host_list(kv_indices, kv_indices_host), P)
     nnz = kv_indices.numel()
     st = lib().attn_fwd_paged(_ptr(q, "q"), _ptr(k_cache, "k_cache"), _ptr(v_cache, "v_cache"),
                               _ptr(o, "o"), _ptr(lse, "lse", torch.float32),
@@ -294,7 +304,17 @@ def attn_decode_paged_workspace_size(batch: int, max_kvlen: int, Hq: int, Hkv: i
 
 def attn_decode_paged(q, k_cache, v_cache, o, lse, kv_indptr, kv_indices, max_kvlen: int,
                       scale: float, workspace: torch.Tensor, stream=None,
-                      kv_indptr_host=None, kv_indices_host=None) -> None:
+                      kv_indptr_host=None, kv_indices_host=None, checked: bool = False) -> None:
+    """Paged decode (see attn_fwd_paged for `checked` and the host copies)."""
+    attn_decode_paged_phases(q, k_cache, v_cache, o, lse, kv_indptr, kv_indices, max_kvlen,
+                             scale, workspace, ATTN_DECODE_SPLIT | ATTN_DECODE_MERGE, stream,
+                             kv_indptr_host, kv_indices_host, checked)
+
+
+def attn_decode_paged_phases(q, k_cache, v_cache, o, lse, kv_indptr, kv_indices, max_kvlen: int,
+                             scale: float, workspace: torch.Tensor, phases: int, stream=None,
+                             kv_indptr_host=None, kv_indices_host=None,
+                             checked: bool = False) -> None:
     batch, Hq, D = q.shape
     P, Hkv = k_cache.shape[0], k_cache.shape[1]
     _shape(k_cache, (P, Hkv, D), "k_cache")
@@ -302,17 +322,17 @@ def attn_decode_paged(q, k_cache, v_cache, o, lse, kv_indptr, kv_indices, max_kv
     _shape(o, (batch, Hq, D), "o")
     _shape(lse, (Hq, batch), "lse")
     _shape(kv_indptr, (batch + 1,), "kv_indptr")
-    check_paged_host(_host_list(kv_indptr, kv_indptr_host),
-                     _host_list(kv_indices, kv_indices_host), P, max_kvlen)
+    if not checked:
+        check_paged_host(_host_list(kv_indptr, kv_indptr_host),
+                         _host_list(kv_indices, kv_indices_host), P, max_kvlen)
     nnz = kv_indices.numel()
-    st = lib().attn_decode_paged(_ptr(q, "q"), _ptr(k_cache, "k_cache"), _ptr(v_cache, "v_cache"),
-                                 _ptr(o, "o"), _ptr(lse, "lse", torch.float32),
-                                 _ptr(kv_indptr, "kv_indptr", torch.int32),
-                                 _ptr(kv_indices, "kv_indices", torch.int32) if nnz else 0,
-                                 batch, int(max_kvlen), nnz, P, Hq, Hkv, D, float(scale),
-                                 _ptr(workspace, "workspace", torch.uint8), workspace.numel(),
-                                 _stream(stream))
-    _check(st, "attn_decode_paged")
+    st = lib().attn_decode_paged_phases(
+        _ptr(q, "q"), _ptr(k_cache, "k_cache"), _ptr(v_cache, "v_cache"), _ptr(o, "o"),
+        _ptr(lse, "lse", torch.float32), _ptr(kv_indptr, "kv_indptr", torch.int32),
+        _ptr(kv_indices, "kv_indices", torch.int32) if nnz else 0, batch, int(max_kvlen), nnz, P,
+        Hq, Hkv, D, float(scale), _ptr(workspace, "workspace", torch.uint8), workspace.numel(),
+        int(phases), _stream(stream))
+    _check(st, "attn_decode_paged_phases")
 
 
 # --------------------------------------------------------------------------

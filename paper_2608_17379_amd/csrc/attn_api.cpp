@@ -279,12 +279,14 @@ size_t attn_decode_paged_workspace_size(int batch, int max_kvlen, int Hq, int Hk
   return round256(slots * D * 4) + round256(slots * 4);
 }
 
-int attn_decode_paged(const void* q, const void* k_cache, const void* v_cache, void* o,
-                      float* lse, const int* kv_indptr, const int* kv_indices, int batch,
-                      int max_kvlen, int nnz, int num_pages, int Hq, int Hkv, int D, float scale,
-                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+int attn_decode_paged_phases(const void* q, const void* k_cache, const void* v_cache, void* o,
+                             float* lse, const int* kv_indptr, const int* kv_indices, int batch,
+                             int max_kvlen, int nnz, int num_pages, int Hq, int Hkv, int D,
+                             float scale, void* workspace, size_t workspace_bytes, int phases,
+                             hipStream_t stream) {
   int st = check_common(Hq, Hkv, D, 0, scale);
   if (st != ATTN_OK) return st;
+  if (phases < 1 || phases > 3) return ATTN_ERR_VALUE;
   if (Hq / Hkv > 32) return ATTN_ERR_GQA;
   if (batch < 0 || check_rows(max_kvlen) != ATTN_OK) return ATTN_ERR_SHAPE;
   if ((st = check_cache(num_pages, nnz, Hkv, D)) != ATTN_OK) return st;
@@ -318,7 +320,16 @@ int attn_decode_paged(const void* q, const void* k_cache, const void* v_cache, v
   const int64_t slots = (int64_t)batch * Hq * a.nchunk;
   a.part_o = static_cast<float*>(workspace);
   a.part_lse = reinterpret_cast<float*>(static_cast<char*>(workspace) + round256(slots * D * 4));
-  return attn::launch_decode(a, D, stream) == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
+  return attn::launch_decode(a, D, phases, stream) == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
+}
+
+int attn_decode_paged(const void* q, const void* k_cache, const void* v_cache, void* o,
+                      float* lse, const int* kv_indptr, const int* kv_indices, int batch,
+                      int max_kvlen, int nnz, int num_pages, int Hq, int Hkv, int D, float scale,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return attn_decode_paged_phases(q, k_cache, v_cache, o, lse, kv_indptr, kv_indices, batch,
+                                  max_kvlen, nnz, num_pages, Hq, Hkv, D, scale, workspace,
+                                  workspace_bytes, ATTN_DECODE_SPLIT | ATTN_DECODE_MERGE, stream);
 }
 
 const char* attn_status_string(int status) {

@@ -9,15 +9,14 @@
 // request's keys are spread over many workgroups to keep the chip's memory
 // system busy:
 //
-//  * decode_split_kernel: one workgroup of 4 wavefronts per (request,
-//    key/value head, chunk of 128 keys).  The rows of the chunk are gathered
-//    from the cache straight into LDS (buffer_load ... lds, one page number per
-//    copied row).  The query heads of the group are the columns of one MFMA
-//    tile: each wavefront computes S^T = K Q^T for 32 keys, the workgroup
-//    agrees on one maximum per query through LDS, and each wavefront adds
-//    P^T into O^T = V^T P^T with V^T read transposed out of the V tile.  The
-//    four partial outputs share that maximum, so they are summed without
-//    rescaling.  A request with one chunk writes its result directly;
+//  * decode_split_kernel: one wavefront per (request, key/value head, chunk
+//    of 64 keys).  The query heads of the group are the columns of one MFMA
+//    tile.  The chunk's K rows are gathered straight into registers as the A
+//    operand of S^T = K Q^T, its V rows into LDS (buffer_load ... lds, one
+//    page number per copied row) for the transposing reads of V^T in
+//    O^T = V^T P^T; with 16 KiB of LDS per wavefront about ten chunks are in
+//    flight on every CU, so the page-number loads and the gathers of all
+//    chunks overlap.  A request with one chunk writes its result directly;
 //    otherwise the chunk's normalised output and log-sum-exp (base 2) go to
 //    the workspace.
 //  * decode_merge_kernel: one wavefront per (request, query head) combines
@@ -30,22 +29,15 @@
 namespace attn {
 namespace {
 
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
-static_assert(kDecodeChunk == 32 * kWaves, "one 32-key block per wavefront");
+static_assert(kDecodeChunk == 64, "one 64-key chunk per wavefront");
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a) {
-  using Tile = AsyncTile<D, kWaves>;
+__global__ __launch_bounds__(64) void decode_split_kernel(DecodeArgs a) {
+  using Tile = AsyncTile<D, 1>;
   constexpr int P = Tile::P;
-  // K tiles (keys 0-63, 64-127) then V tiles; reused for the cross-wavefront
-  // sum of O^T once every wavefront has finished reading them.
-  __shared__ __attribute__((aligned(1024))) uint16_t smem[4 * Tile::ELEMS];
-  __shared__ float red_m[kWaves][32];
-  __shared__ float red_l[kWaves][32];
+  __shared__ __attribute__((aligned(1024))) uint16_t sv[Tile::ELEMS];   // the chunk's V rows
 
-  const int lane = threadIdx.x & 63, wave = wave_id();
-  const int l32 = lane & 31, half = lane >> 5;
+  const int lane = threadIdx.x, l32 = lane & 31, half = lane >> 5;
   const int z = blockIdx.x / a.Hkv, hk = blockIdx.x % a.Hkv;
   const int chunk = blockIdx.y;
   const int G = a.group;
@@ -58,15 +50,14 @@ __global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a)
   if (k0 >= len) return;
   const int nch = (len + kDecodeChunk - 1) / kDecodeChunk;
 
-  // Page numbers of this lane's rows in the four tile copies (the same rows
-  // for K and V).
+  // Lane i fetches the page of key k0 + i; other lanes' pages come by
+  // cross-lane reads.  Keys past the end and pages outside the cache read
+  // as zero rows.
   const rsrc_t ixr = make_rsrc(a.kv_idx + ks, (int64_t)len * 4);
-  int pidx[2][Tile::NJ];
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int j = 0; j < Tile::NJ; ++j)
-      pidx[t][j] = bload4(ixr, 4 * (k0 + 64 * t + Tile::row_of(wave, j, lane)));
+  const int page = bload4(ixr, 4 * (k0 + lane));
+  const bool ok = k0 + lane < len && (unsigned)page < (unsigned)a.num_pages;
+  const int row_bytes = a.Hkv * D * 2;
+  const int my_off = ok ? page * row_bytes : kPadOffset;
 
   // Q^T as the B operand: column l32 is query head hk * G + l32 of the
   // request; columns >= G read as zero.
@@ -76,123 +67,124 @@ __global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a)
 #pragma unroll
   for (int c = 0; c < D / 16; ++c) qreg[c] = bload16(rq, l32 * D * 2 + 16 * half + 32 * c);
 
-  const int row_bytes = a.Hkv * D * 2;
   const int64_t cache_bytes = (int64_t)a.num_pages * row_bytes - (int64_t)hk * D * 2;
   const rsrc_t kc = make_rsrc(a.k + (int64_t)hk * D, cache_bytes);
   const rsrc_t vc = make_rsrc(a.v + (int64_t)hk * D, cache_bytes);
-  const Tile dma(wave, lane, 0);
-#pragma unroll
-  for (int t = 0; t < 2; ++t) {
+
+  // V rows gathered into LDS (DMA instruction j copies tile rows 4j + lane/16
+  // at D = 128), K rows straight into registers as the A operand of
+  // S^T = K Q^T: block b holds keys 32b + l32, 16 bytes at column 16c + 8 half.
+  {
+    const Tile dma(0, lane, 0);
     int off[Tile::NJ];
 #pragma unroll
     for (int j = 0; j < Tile::NJ; ++j) {
-      const int key = k0 + 64 * t + Tile::row_of(wave, j, lane);
-      off[j] = Tile::gather_off(wave, j, lane, pidx[t][j], key < len, a.num_pages, row_bytes);
+      const int c = Tile::chunk_of(0, j, lane);
+      const int ro = __shfl(my_off, Tile::row_of(0, j, lane));
+      off[j] = c < D / 8 ? ro + 16 * c : kPadOffset;
     }
-    dma.load_at(kc, off, smem + t * Tile::ELEMS, wave);
-    dma.load_at(vc, off, smem + (2 + t) * Tile::ELEMS, wave);
+    dma.load_at(vc, off, sv, 0);
   }
-  wait_vm<0>();
-  __syncthreads();
+  u32x4 kreg[2][D / 16];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int ro = __shfl(my_off, 32 * b + l32);
+#pragma unroll
+    for (int c = 0; c < D / 16; ++c) kreg[b][c] = bload16(kc, ro + 16 * half + 32 * c);
+  }
 
-  // S^T for this wavefront's keys kw0 .. kw0 + 31 (tile wave / 2).
-  const int kw0 = k0 + 32 * wave;
-  const RowReader<D> rr(l32, half);
-  const uint16_t* kt = smem + (wave >> 1) * Tile::ELEMS + 32 * (wave & 1) * P;
-  f32x16 s;
+  f32x16 s[2];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) s[r] = 0.f;
+  for (int b = 0; b < 2; ++b) {
 #pragma unroll
-  for (int c = 0; c < D / 16; ++c) s = mfma32(ld16(kt + rr.rm[c]), qreg[c], s);
-  // s[r]: key kw0 + 8(r/4) + 4half + r%4, query column l32.
+    for (int r = 0; r < 16; ++r) s[b][r] = 0.f;
+#pragma unroll
+    for (int c = 0; c < D / 16; ++c) s[b] = mfma32(kreg[b][c], qreg[c], s[b]);
+  }
+  // s[b][r]: key k0 + 32b + 8(r/4) + 4half + r%4, query column l32.
   float mx = -INFINITY;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int key = kw0 + 8 * (r / 4) + 4 * half + (r % 4);
-    s[r] = key < len ? s[r] : -INFINITY;
-    mx = fmaxf(mx, s[r]);
-  }
-  mx = fmaxf(mx, swap_halves(mx));
-  if (half == 0) red_m[wave][l32] = mx;
-  __syncthreads();
-  float m = red_m[0][l32];
+  for (int b = 0; b < 2; ++b)
 #pragma unroll
-  for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red_m[w][l32]);
-  const float mt = m * a.scale_log2;   // the chunk's row maximum, exp2 units (finite)
+    for (int r = 0; r < 16; ++r) {
+      const int key = k0 + 32 * b + 8 * (r / 4) + 4 * half + (r % 4);
+      s[b][r] = key < len ? s[b][r] : -INFINITY;
+      mx = fmaxf(mx, s[b][r]);
+    }
+  mx = fmaxf(mx, swap_halves(mx));
+  const float mt = mx * a.scale_log2;   // the chunk's row maximum, exp2 units (finite)
   float ls = 0.f;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    s[r] = fast_exp2(__builtin_fmaf(s[r], a.scale_log2, -mt));
-    ls += s[r];
-  }
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      s[b][r] = fast_exp2(__builtin_fmaf(s[b][r], a.scale_log2, -mt));
+      ls += s[b][r];
+    }
   ls += swap_halves(ls);
 
-  // O^T[d][q] += sum over this wavefront's keys of V^T[d][key] P^T[key][q].
+  // O^T[d][q] = sum over the chunk's keys of V^T[d][key] P^T[key][q], V^T
+  // read transposed out of the V tile (chunk c of block b = tile rows
+  // 32b + 16c .. + 15).
+  wait_vm<0>();   // the V rows have landed (one wavefront: no barrier needed)
   const TransReader<D> tr(lane);
-  const uint16_t* vt = smem + (2 + (wave >> 1)) * Tile::ELEMS;
   f32x16 oacc[D / 32];
 #pragma unroll
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    const u32x4 pb = pack_chunk(s, c);
-    const int rc = 16 * (2 * (wave & 1) + c) * P;
+  for (int b = 0; b < 2; ++b)
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-      const u32x2 lo = ld_tr(vt + tr.tr[db][0] + rc), hi = ld_tr(vt + tr.tr[db][1] + rc);
-      oacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb, oacc[db]);
+    for (int c = 0; c < 2; ++c) {
+      const u32x4 pb = pack_chunk(s[b], c);
+      const int rc = 16 * (2 * b + c) * P;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        const u32x2 lo = ld_tr(sv + tr.tr[db][0] + rc), hi = ld_tr(sv + tr.tr[db][1] + rc);
+        oacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb, oacc[db]);
+      }
     }
-  }
 
-  // Sum over the wavefronts: each writes its G valid columns, [wave][g][D]
-  // fp32 (at most 4 x 32 x D x 4 bytes, within the tile buffer).
-  __syncthreads();   // every wavefront is done with the tiles
-  float* red_o = reinterpret_cast<float*>(smem);
-  if (l32 < G) {
-    float* dst = red_o + ((int64_t)wave * G + l32) * D;
+  // Lane (l32, half) holds column l32 (query head hk G + l32) at rows
+  // 32 db + 8 i + 4 half + 0..3.
+  if (l32 >= G) return;
+  const float inv = 1.f / ls;   // ls >= 1: the maximum's own key contributes 1
+  const float lse2 = mt + log2f(ls);
+  const int64_t h = (int64_t)hk * G + l32;
+  if (nch == 1) {
+    uint16_t* op = a.o + ((int64_t)z * a.Hq + h) * D + 4 * half;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
-        *reinterpret_cast<f32x4*>(dst + 32 * db + 8 * g + 4 * half) =
-            f32x4{oacc[db][4 * g], oacc[db][4 * g + 1], oacc[db][4 * g + 2], oacc[db][4 * g + 3]};
-  }
-  if (half == 0) red_l[wave][l32] = ls;
-  __syncthreads();
-
-  const int64_t hq0 = (int64_t)hk * G;
-  for (int i = threadIdx.x; i < G * (D / 4); i += kThreads) {
-    const int g = i / (D / 4), d = 4 * (i % (D / 4));
-    f32x4 acc = *reinterpret_cast<const f32x4*>(red_o + (int64_t)g * D + d);
-    float l = red_l[0][g], mg = red_m[0][g];
+      for (int i = 0; i < 4; ++i)
+        st8(op + 32 * db + 8 * i,
+            u32x2{pack_bf16(oacc[db][4 * i] * inv, oacc[db][4 * i + 1] * inv),
+                  pack_bf16(oacc[db][4 * i + 2] * inv, oacc[db][4 * i + 3] * inv)});
+    if (half == 0) a.lse[h * a.batch + z] = lse2 * kLn2;
+  } else {
+    const int64_t slot = ((int64_t)z * a.Hq + h) * a.nchunk + chunk;
+    float* po = a.part_o + slot * D + 4 * half;
 #pragma unroll
-    for (int w = 1; w < kWaves; ++w) {
-      const f32x4 x = *reinterpret_cast<const f32x4*>(red_o + ((int64_t)w * G + g) * D + d);
-      acc += x;
-      l += red_l[w][g];
-      mg = fmaxf(mg, red_m[w][g]);
-    }
-    const float inv = 1.f / l;   // l >= 1: the maximum's own key contributes 1
-    const float lse2 = mg * a.scale_log2 + log2f(l);
-    const int64_t h = hq0 + g;
-    if (nch == 1) {
-      uint16_t* op = a.o + ((int64_t)z * a.Hq + h) * D + d;
-      st8(op, u32x2{pack_bf16(acc[0] * inv, acc[1] * inv), pack_bf16(acc[2] * inv, acc[3] * inv)});
-      if (d == 0) a.lse[h * a.batch + z] = lse2 * kLn2;
-    } else {
-      const int64_t slot = ((int64_t)z * a.Hq + h) * a.nchunk + chunk;
-      *reinterpret_cast<f32x4*>(a.part_o + slot * D + d) = acc * inv;
-      if (d == 0) a.part_lse[slot] = lse2;
-    }
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        *reinterpret_cast<f32x4*>(po + 32 * db + 8 * i) =
+            f32x4{oacc[db][4 * i], oacc[db][4 * i + 1], oacc[db][4 * i + 2], oacc[db][4 * i + 3]} *
+            inv;
+    if (half == 0) a.part_lse[slot] = lse2;
   }
 }
 
-// One wavefront per (request, query head); lane l handles output columns
-// 4l .. 4l + 3.
+// One wavefront per (request, query head).  The chunks' log-sum-exps are
+// read one per lane (64 chunks at a time) and reduced across the wavefront;
+// then lane group gq = lane / CW takes chunks gq, gq + NG, ... and lane
+// l % CW output columns 4 (l % CW) .. + 3 (lanes past column D idle), and
+// the groups' sums are added with cross-lane exchanges.
 template <int D>
 __global__ __launch_bounds__(64) void decode_merge_kernel(DecodeArgs a) {
+  constexpr int CW = D / 4 <= 16 ? 16 : 32;   // lanes per output row (a power of two)
+  constexpr int NG = 64 / CW;                 // lane groups
   const int lane = threadIdx.x;
   const int z = blockIdx.x / a.Hq, h = blockIdx.x % a.Hq;
   int ks = a.kv_cu[z], ke = a.kv_cu[z + 1];
@@ -201,25 +193,39 @@ __global__ __launch_bounds__(64) void decode_merge_kernel(DecodeArgs a) {
   const int len = min(ke - ks, a.max_kvlen);
   const int nch = (len + kDecodeChunk - 1) / kDecodeChunk;
   if (nch == 1) return;   // written by the split kernel
-  const int d = 4 * lane;
+  const int gq = lane / CW, d = 4 * (lane % CW);
+  const bool col = d < D;
   uint16_t* op = a.o + ((int64_t)z * a.Hq + h) * D + d;
   if (nch == 0) {   // no keys: O = 0, L = -inf
-    if (d < D) st8(op, u32x2{0u, 0u});
+    if (gq == 0 && col) st8(op, u32x2{0u, 0u});
     if (lane == 0) a.lse[(int64_t)h * a.batch + z] = -INFINITY;
     return;
   }
   const int64_t slot0 = ((int64_t)z * a.Hq + h) * a.nchunk;
   float M = -INFINITY;
-  for (int c = 0; c < nch; ++c) M = fmaxf(M, a.part_lse[slot0 + c]);
+  for (int c0 = 0; c0 < nch; c0 += 64)
+    if (c0 + lane < nch) M = fmaxf(M, a.part_lse[slot0 + c0 + lane]);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   float wsum = 0.f;
-  for (int c = 0; c < nch; ++c) {
-    const float w = fast_exp2(a.part_lse[slot0 + c] - M);
-    wsum += w;
-    if (d < D) acc += w * *reinterpret_cast<const f32x4*>(a.part_o + (slot0 + c) * D + d);
+  for (int c0 = 0; c0 < nch; c0 += 64) {
+    const float wl = c0 + lane < nch ? fast_exp2(a.part_lse[slot0 + c0 + lane] - M) : 0.f;
+    wsum += wl;
+    const int n = min(64, nch - c0);
+    for (int c = gq; c < n; c += NG) {
+      const float w = __shfl(wl, c);
+      if (col) acc += w * *reinterpret_cast<const f32x4*>(a.part_o + (slot0 + c0 + c) * D + d);
+    }
   }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) wsum += __shfl_xor(wsum, o);
+#pragma unroll
+  for (int o = CW; o < 64; o <<= 1)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] += __shfl_xor(acc[i], o);
   const float inv = 1.f / wsum;
-  if (d < D)
+  if (gq == 0 && col)
     st8(op, u32x2{pack_bf16(acc[0] * inv, acc[1] * inv), pack_bf16(acc[2] * inv, acc[3] * inv)});
   if (lane == 0) a.lse[(int64_t)h * a.batch + z] = (M + log2f(wsum)) * kLn2;
 }
@@ -232,22 +238,25 @@ template __global__ void decode_merge_kernel<96>(DecodeArgs);
 template __global__ void decode_merge_kernel<128>(DecodeArgs);
 
 template <int D>
-void launch_decode_d(const DecodeArgs& a, hipStream_t stream) {
-  const dim3 gs((unsigned)(a.batch * a.Hkv), (unsigned)a.nchunk);
-  hipLaunchKernelGGL((decode_split_kernel<D>), gs, dim3(kThreads), 0, stream, a);
-  hipLaunchKernelGGL((decode_merge_kernel<D>), dim3((unsigned)(a.batch * a.Hq)), dim3(64), 0,
-                     stream, a);
+void launch_decode_d(const DecodeArgs& a, int phases, hipStream_t stream) {
+  if (phases & 1) {
+    const dim3 gs((unsigned)(a.batch * a.Hkv), (unsigned)a.nchunk);
+    hipLaunchKernelGGL((decode_split_kernel<D>), gs, dim3(64), 0, stream, a);
+  }
+  if (phases & 2)
+    hipLaunchKernelGGL((decode_merge_kernel<D>), dim3((unsigned)(a.batch * a.Hq)), dim3(64), 0,
+                       stream, a);
 }
 
 }  // namespace
 
-hipError_t launch_decode(const DecodeArgs& a, int D, hipStream_t stream) {
+hipError_t launch_decode(const DecodeArgs& a, int D, int phases, hipStream_t stream) {
   if (D == 64)
-    launch_decode_d<64>(a, stream);
+    launch_decode_d<64>(a, phases, stream);
   else if (D == 96)
-    launch_decode_d<96>(a, stream);
+    launch_decode_d<96>(a, phases, stream);
   else
-    launch_decode_d<128>(a, stream);
+    launch_decode_d<128>(a, phases, stream);
   return hipGetLastError();
 }
 

@@ -86,8 +86,9 @@ struct DecodeArgs {
 // Launchers: enqueue on `stream`, return the hipGetLastError() of the launch.
 hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream);
 // Keys per chunk of the decode split (sizes the workspace).
-constexpr int kDecodeChunk = 128;
-hipError_t launch_decode(const DecodeArgs& a, int D, hipStream_t stream);
+constexpr int kDecodeChunk = 64;
+// phases: bit 0 = split kernel, bit 1 = merge kernel.
+hipError_t launch_decode(const DecodeArgs& a, int D, int phases, hipStream_t stream);
 // phases: bit 0 = Delta and dQ kernel, bit 1 = dK/dV kernel.
 hipError_t launch_bwd(const BwdArgs& a, int D, int phases, hipStream_t stream);
 

@@ -209,3 +209,10 @@ def test_paged_host_check():
                            ([0, 3], [0, 1, 2], 5, 2), ([0, 2], [0, 1, 2], 5, None)):
         with pytest.raises(ValueError):
             attn.check_paged_host(kv, idx, p, mk)
+
+
+def test_decode_phase_mask_validation():
+    l = attn.lib()
+    args = [A] * 7 + [3, 500, 900, 1000, 24, 8, 128, 0.1, A, 1 << 24]
+    for bad in (0, 4, -1):
+        assert l.attn_decode_paged_phases(*args, bad, None) == -8

@@ -3,7 +3,7 @@ oracle: paged prefill through attn_fwd_paged and decode through
 attn_decode_paged, called through the C ABI by the binding.
 
 Small cases span several key tiles (64 keys forward), several decode chunks
-(128 keys) and ragged tails, with head dimensions 64, 96 and 128, grouped
+(64 keys) and ragged tails, with head dimensions 64, 96 and 128, grouped
 query heads, requests with fewer queries than keys, and empty requests.  The
 paper's two paged workloads run at full size, compared on every head.
 """
@@ -87,8 +87,9 @@ def _decode(q, kc, vc, kv, idx, max_kvlen, scale, label):
 @pytest.mark.parametrize("D", [64, 96, 128])
 @pytest.mark.parametrize("Hq,Hkv", [(4, 4), (24, 8), (32, 4), (32, 1)])
 def test_paged_decode(D, Hq, Hkv):
-    # one chunk, exactly one and two chunks, a ragged tail, many chunks, no keys
-    kv_lens = [1, 127, 128, 129, 700, 0, 256]
+    # one key, one chunk (64 keys) and its neighbours, two chunks and their
+    # neighbours, many chunks, no keys
+    kv_lens = [1, 63, 64, 65, 127, 128, 129, 700, 0, 256]
     q, kc, vc, _, kv, idx = _draw(2, [1] * len(kv_lens), kv_lens, Hq, Hkv, D, 4000)
     announce(f"paged decode D={D} Hq={Hq} Hkv={Hkv}")
     _decode(q, kc, vc, kv, idx, max(kv_lens), D ** -0.5, f"decode d{D} g{Hq // Hkv}")

@@ -7,7 +7,8 @@ Without --workload it measures the headline workload (B4 H16 S2048 D128
 causal).  The paged-cache workloads (paged prefill, paged decode) are forward
 only, as in the paper: their step is one attn_fwd_paged call (TFLOP/s) or one
 attn_decode_paged call (its split and merge kernels; HBM GB/s, with the
-roofline against 8 TB/s since decode reads each key and value once).
+roofline against 8 TB/s since decode reads each key and value once).  The
+GEMM workload's step is one attn_gemm_bf16_nt call (2 M N K FLOP).
 
 A step is one forward (attn_fwd) and one backward (attn_bwd_phases with the
 Delta/dQ phase, then the dK/dV phase: together exactly attn_bwd) over one
@@ -58,7 +59,7 @@ KERNELS = ("fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel")
 GEMMS = {"fwd_kernel": 2, "bwd_dq_kernel": 3, "bwd_dkdv_kernel": 4}
 KERNEL_SOURCES = {"fwd_kernel": "attn_fwd.hip", "bwd_dq_kernel": "attn_bwd.hip",
                   "bwd_dkdv_kernel": "attn_bwd.hip", "decode_split_kernel": "attn_decode.hip",
-                  "decode_merge_kernel": "attn_decode.hip"}
+                  "decode_merge_kernel": "attn_decode.hip", "gemm_nt_kernel": "gemm.hip"}
 
 
 def fwd_flops(w, cu_seqlens=None) -> float:
@@ -301,6 +302,84 @@ def run_paged(args, w) -> int:
     return 0
 
 
+# ---------------------------------------------------------------------------
+# BF16 GEMM C = A B^T
+# ---------------------------------------------------------------------------
+
+def run_gemm(args, w) -> int:
+    import torch
+    import oracle
+    from paper_2608_17379_amd import attn
+    from paper_2608_17379_amd import workloads as wl
+
+    a_h, b_h = wl.make_gemm_inputs(w, 0)
+    dev = torch.device("cuda", 0)
+    a, b = a_h.to(dev), b_h.to(dev)
+    c = torch.empty(w.M, w.N, dtype=torch.bfloat16, device=dev)
+    lib = attn.lib()
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        st = lib.attn_gemm_bf16_nt(a.data_ptr(), b.data_ptr(), c.data_ptr(), w.M, w.N, w.K,
+                                   stream)
+        if st != 0:
+            raise attn.AttnError(st, "attn_gemm_bf16_nt")
+        if ev is not None:
+            ev[1].record()
+
+    attn.attn_gemm_bf16_nt(a, b, c)   # shape and pointer checks once, through the binding
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)]
+           for _ in range(max(args.steps, args.warmup))]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.warmup):
+        step(evs[i])
+    host_ms = (time.perf_counter() - t0) * 1e3 / max(1, args.warmup)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    hold_gpu_for_enqueue(host_ms, args.steps)
+    start.record()
+    for i in range(args.steps):
+        step(evs[i])
+    end.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(end) / args.steps
+    kern_ms = sum(e[0].elapsed_time(e[1]) for e in evs[:args.steps]) / args.steps
+    if not torch.isfinite(c.float()).all():
+        print("non-finite output", file=sys.stderr)
+        return 1
+    F = 2.0 * w.M * w.N * w.K
+    ach = F / (kern_ms * 1e-3) / 1e12
+    rec = {"metric": f"bf16 GEMM TFLOP/s, {w.name}",
+           "value": round(F / (ms_step * 1e-3) / 1e12, 2), "unit": "TFLOP/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 5),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (seeded i.i.d. N(0,1) bf16)",
+           "config": {"workload": w.name, "M": w.M, "N": w.N, "K": w.K, "seed": 0},
+           "pct_peak": round(100 * F / (ms_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+           "kernel_ms": {"gemm_nt_kernel": round(kern_ms, 5)},
+           "roofline": {"kernel": "gemm_nt_kernel", "bound": "mfma", "achieved": round(ach, 2),
+                        "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                        "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                        "traffic": load_traffic("gemm_nt_kernel", w.name)},
+           "cpu_baseline": None}
+    if not args.no_cpu_baseline:
+        # The oracle on whole rows of C (64 rows at a time) until the budget is spent.
+        t0, rows = time.perf_counter(), 0
+        while rows == 0 or time.perf_counter() - t0 < args.cpu_seconds:
+            r0 = rows % w.M
+            oracle.gemm_nt(a_h[r0:r0 + 64], b_h)
+            rows += 64
+        dt = time.perf_counter() - t0
+        rec["cpu_baseline"] = {"value": round(2.0 * rows * w.N * w.K / dt / 1e12, 6),
+                               "unit": "TFLOP/s", "cores": torch.get_num_threads(),
+                               "kind": "oracle",
+                               "sample": f"{rows} rows of C ({rows}x{w.N}x{w.K}), fp64, {dt:.1f} s"}
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
 def copy_calibration(nbytes: int, reps: int) -> None:
     """A plain device copy of known size, for scaling HBM byte counters."""
     import torch
@@ -342,9 +421,12 @@ def main(argv=None) -> int:
     name = args.workload or wl.HEADLINE
     if name in wl.PAGED_WORKLOADS:
         return run_paged(args, wl.PAGED_WORKLOADS[name])
+    if name in wl.GEMM_WORKLOADS:
+        return run_gemm(args, wl.GEMM_WORKLOADS[name])
     if name not in wl.WORKLOADS:
         print(f"unknown workload {name}; known: "
-              + ", ".join(list(wl.WORKLOADS) + list(wl.PAGED_WORKLOADS)), file=sys.stderr)
+              + ", ".join(list(wl.WORKLOADS) + list(wl.PAGED_WORKLOADS)
+                          + list(wl.GEMM_WORKLOADS)), file=sys.stderr)
         return 2
     w = wl.WORKLOADS[name]
     x = wl.make_inputs(w, 0)

@@ -225,6 +225,19 @@ int attn_decode_paged_phases(const void* q, const void* k_cache, const void* v_c
                              int Hkv, int D, float scale, void* workspace,
                              size_t workspace_bytes, int phases, hipStream_t stream);
 
+/*
+ * BF16 GEMM C = A B^T (the fifth primary workload of PTXBench, Appendix A,
+ * "Workloads": A 8192 x 5120, B 7168 x 5120, C 8192 x 7168).  a [M, K],
+ * b [N, K], c [M, N], all row-major bf16 and 16-byte aligned; fp32
+ * accumulation, C rounded to bf16 (round to nearest even).  K and N must be
+ * multiples of 8 and K * 512 below 2^31 (ATTN_ERR_SHAPE); M is free.
+ * K == 0 gives C = 0 (a and b may then be null); M == 0 or N == 0 is a
+ * no-op (every pointer may then be null).
+ * Ownership, asynchrony and errors as for the attention calls.
+ */
+int attn_gemm_bf16_nt(const void* a, const void* b, void* c, int M, int N, int K,
+                      hipStream_t stream);
+
 /* Static, human-readable text for a status code (never null). */
 const char* attn_status_string(int status);
 

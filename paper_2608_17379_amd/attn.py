@@ -26,7 +26,8 @@ STATUS_NAMES = {
 EXPORTS = ("attn_fwd", "attn_bwd", "attn_bwd_workspace_size", "attn_fwd_varlen",
            "attn_bwd_varlen", "attn_bwd_varlen_workspace_size", "attn_bwd_phases",
            "attn_bwd_varlen_phases", "attn_fwd_paged", "attn_decode_paged_workspace_size",
-           "attn_decode_paged", "attn_decode_paged_phases", "attn_status_string")
+           "attn_decode_paged", "attn_decode_paged_phases", "attn_gemm_bf16_nt",
+           "attn_status_string")
 ATTN_BWD_DQ = 1
 ATTN_BWD_DKDV = 2
 ATTN_DECODE_SPLIT = 1
@@ -74,6 +75,8 @@ def lib() -> ctypes.CDLL:
         l.attn_decode_paged.restype = _I
         l.attn_decode_paged_phases.argtypes = [_P] * 7 + [_I] * 7 + [_F, _P, _Z, _I, _P]
         l.attn_decode_paged_phases.restype = _I
+        l.attn_gemm_bf16_nt.argtypes = [_P, _P, _P, _I, _I, _I, _P]
+        l.attn_gemm_bf16_nt.restype = _I
         l.attn_status_string.argtypes = [_I]
         l.attn_status_string.restype = ctypes.c_char_p
         _lib = l
@@ -333,6 +336,27 @@ def attn_decode_paged_phases(q, k_cache, v_cache, o, lse, kv_indptr, kv_indices,
         Hq, Hkv, D, float(scale), _ptr(workspace, "workspace", torch.uint8), workspace.numel(),
         int(phases), _stream(stream))
     _check(st, "attn_decode_paged_phases")
+
+
+# --------------------------------------------------------------------------
+# BF16 GEMM C = A B^T
+# --------------------------------------------------------------------------
+
+def attn_gemm_bf16_nt(a, b, c, stream=None) -> None:
+    M, K = a.shape
+    N = b.shape[0]
+    _shape(b, (N, K), "b")
+    _shape(c, (M, N), "c")
+    st = lib().attn_gemm_bf16_nt(_ptr(a, "a"), _ptr(b, "b"), _ptr(c, "c"), M, N, K,
+                                 _stream(stream))
+    _check(st, "attn_gemm_bf16_nt")
+
+
+def gemm_nt(a, b):
+    """Return C = A B^T (bf16) for A [M, K], B [N, K]."""
+    c = torch.empty((a.shape[0], b.shape[0]), dtype=torch.bfloat16, device=a.device)
+    attn_gemm_bf16_nt(a, b, c)
+    return c
 
 
 # --------------------------------------------------------------------------

@@ -332,6 +332,31 @@ int attn_decode_paged(const void* q, const void* k_cache, const void* v_cache, v
                                   workspace_bytes, ATTN_DECODE_SPLIT | ATTN_DECODE_MERGE, stream);
 }
 
+int attn_gemm_bf16_nt(const void* a, const void* b, void* c, int M, int N, int K,
+                      hipStream_t stream) {
+  if (M < 0 || N < 0 || K < 0) return ATTN_ERR_SHAPE;
+  if (K % 8 != 0 || N % 8 != 0) return ATTN_ERR_SHAPE;
+  // 256 rows of an operand must fit the 31-bit offsets of the buffer loads,
+  // and the grid must fit one dimension.
+  if ((int64_t)K * 2 * 256 > 0x7fffffff) return ATTN_ERR_SHAPE;
+  const int64_t tiles = ((int64_t)M + 255) / 256 * (((int64_t)N + 255) / 256);
+  if (tiles > 0x7fffffff) return ATTN_ERR_SHAPE;
+  if (M == 0 || N == 0) return ATTN_OK;
+  // With K == 0 the operands are empty (C = 0) and may be null.
+  if (!c || (K > 0 && (!a || !b))) return ATTN_ERR_NULL;
+  if (any_misaligned({a, b, c})) return ATTN_ERR_ALIGN;
+  attn::GemmArgs g;
+  g.a = static_cast<const uint16_t*>(a);
+  g.b = static_cast<const uint16_t*>(b);
+  g.c = static_cast<uint16_t*>(c);
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.tiles_m = (M + 255) / 256;
+  g.tiles_n = (N + 255) / 256;
+  return attn::launch_gemm(g, stream) == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
+}
+
 const char* attn_status_string(int status) {
   switch (status) {
     case ATTN_OK: return "ok";

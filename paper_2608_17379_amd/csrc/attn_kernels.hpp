@@ -83,7 +83,18 @@ struct DecodeArgs {
   float* part_lse;         // workspace [batch, Hq, nchunk] fp32, log2 units
 };
 
+// BF16 GEMM C = A B^T: A [M, K], B [N, K], C [M, N], row-major, K % 8 == 0,
+// N % 8 == 0; tiles of 256 x 256.
+struct GemmArgs {
+  const uint16_t* a;
+  const uint16_t* b;
+  uint16_t* c;
+  int M, N, K;
+  int tiles_m, tiles_n;
+};
+
 // Launchers: enqueue on `stream`, return the hipGetLastError() of the launch.
+hipError_t launch_gemm(const GemmArgs& g, hipStream_t stream);
 hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream);
 // Keys per chunk of the decode split (sizes the workspace).
 constexpr int kDecodeChunk = 64;

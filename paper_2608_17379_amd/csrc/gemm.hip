@@ -1,0 +1,164 @@
+// BF16 GEMM C = A B^T for gfx950 (the fifth primary workload of PTXBench,
+// Appendix A, "Workloads": A [M, K], B [N, K], C [M, N], all bf16, both
+// operands with the reduction index contiguous), fp32 accumulation on MFMA.
+//
+// One workgroup of 8 wavefronts per 256 x 256 tile of C, one workgroup per
+// CU.  Each K step of 64 copies the A and B tiles (256 rows x 128 bytes
+// each) straight from global memory into a two-stage LDS ring
+// (buffer_load ... lds, issued a step ahead), in the swizzled row-major
+// layout of the attention kernels, so that every MFMA operand is one
+// conflict-free 16-byte LDS read.  Wavefront (wm, wn) owns rows
+// 128 wm .. + 127 of the tile and columns 64 wn .. + 63, as 4 x 2 blocks of
+// 32 x 32, and computes them transposed (C^T block = B rows x A rows), so
+// that each lane holds four consecutive columns of one row of C and stores
+// them as 8 bytes.
+//
+// Tiles are assigned XCD by XCD: the hardware hands workgroup ids to the 8
+// XCDs in turn, so workgroup b runs on XCD b % 8; the tiles are numbered so
+// that each XCD receives a contiguous range, walked in bands of 4 row tiles
+// (all column tiles of the band, four rows at a time), which keeps the A and
+// B slabs of the tiles running together on one XCD in its L2.
+//
+// Rows past M or N read as zero through buffer-range checks and are not
+// stored; a K that is not a multiple of 64 reads zeros past K (K is a
+// multiple of 8, so every 16-byte chunk is wholly inside or outside).
+#include "attn_kernels.hpp"
+#include "device_common.hpp"
+
+namespace attn {
+namespace {
+
+constexpr int kTM = 256, kTN = 256, kTK = 64;
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kBand = 4;   // row tiles per band of the tile order
+
+using GTile = AsyncTile<64, kWaves>;   // one [64 rows][64 k] sub-tile per DMA instruction
+static_assert(GTile::NJ == 1, "one DMA instruction per wavefront per 64-row sub-tile");
+constexpr int kSubElems = GTile::ELEMS;            // 4096 bf16
+constexpr int kTileElems = 4 * kSubElems;          // 256 rows
+
+template <bool KTAIL>
+__global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(1024))) uint16_t sa0[kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sb0[kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sa1[kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sb1[kTileElems];
+
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int l32 = lane & 31, half = lane >> 5;
+
+  // Tile of this workgroup.
+  const int nblk = (int)gridDim.x, bid = (int)blockIdx.x;
+  const int t = nblk % 8 == 0 ? (bid % 8) * (nblk / 8) + bid / 8 : bid;
+  const int band_tiles = kBand * g.tiles_n;
+  const int m_first = (t / band_tiles) * kBand;
+  const int band_rows = min(kBand, g.tiles_m - m_first);
+  const int tb = t % band_tiles;
+  const int m0 = (m_first + tb % band_rows) * kTM;
+  const int n0 = (tb / band_rows) * kTN;
+
+  const int K = g.K;
+  const int row_bytes = K * 2;
+  const rsrc_t ra = make_rsrc(g.a + (int64_t)m0 * K, (int64_t)(g.M - m0) * row_bytes);
+  const rsrc_t rb = make_rsrc(g.b + (int64_t)n0 * K, (int64_t)(g.N - n0) * row_bytes);
+
+  // This lane's DMA source: row r = 8 wave + lane / 8 of every 64-row
+  // sub-tile, logical 16-byte chunk lg (k = 8 lg .. 8 lg + 7 of the step).
+  const int drow = GTile::row_of(wave, 0, lane);
+  const int lg = GTile::chunk_of(wave, 0, lane);
+  const int doff = drow * row_bytes + 16 * lg;
+
+  auto load = [&](int kt, uint16_t* da, uint16_t* db) __attribute__((always_inline)) {
+    const int k0 = kt * kTK;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      int off = doff + 64 * s * row_bytes + 2 * k0;
+      if constexpr (KTAIL) off = k0 + 8 * lg < K ? off : kPadOffset;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          ra, (ATTN_LDS void*)(da + s * kSubElems + wave * 64 * 8), 16, off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rb, (ATTN_LDS void*)(db + s * kSubElems + wave * 64 * 8), 16, off, 0, 0, 0);
+    }
+  };
+
+  const int wm = wave >> 2, wn = wave & 3;
+  const RowReader<64> rr(l32, half);
+  // 32-row block q of a 256-row tile starts at element q * 2048 (sub-tile
+  // q / 2, row 32 (q % 2)); the swizzle depends on the row modulo 16 only.
+  f32x16 acc[2][4];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
+
+  auto compute = [&](const uint16_t* sa, const uint16_t* sb) __attribute__((always_inline)) {
+#pragma unroll
+    for (int c = 0; c < kTK / 16; ++c) {
+      u32x4 bo[2], ao[4];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) bo[j] = ld16(sb + (2 * wn + j) * 2048 + rr.rm[c]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ao[i] = ld16(sa + (4 * wm + i) * 2048 + rr.rm[c]);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[j][i] = mfma32(bo[j], ao[i], acc[j][i]);
+    }
+  };
+
+  const int nkt = (K + kTK - 1) / kTK;
+  // Step kt: wait for its copies (this wavefront's, then everyone's through
+  // the barrier, which also frees the stage read at kt - 1), start the copies
+  // of kt + 1 into that stage, then compute.
+  auto step = [&](int kt, const uint16_t* ca, const uint16_t* cb, uint16_t* na, uint16_t* nb)
+      __attribute__((always_inline)) {
+    wait_vm<0>();
+    __syncthreads();
+    if (kt + 1 < nkt) load(kt + 1, na, nb);
+    compute(ca, cb);
+  };
+  if (nkt > 0) load(0, sa0, sb0);
+  int kt = 0;
+  for (; kt + 1 < nkt; kt += 2) {
+    step(kt, sa0, sb0, sa1, sb1);
+    step(kt + 1, sa1, sb1, sa0, sb0);
+  }
+  if (kt < nkt) step(kt, sa0, sb0, sa1, sb1);
+
+  // acc[j][i] is the C^T block of columns n0 + 64 wn + 32 j + (8 (r/4) +
+  // 4 half + r%4) and row m0 + 128 wm + 32 i + l32.
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + 128 * wm + 32 * i + l32;
+    if (m >= g.M) continue;
+    uint16_t* crow = g.c + (int64_t)m * g.N;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int n = n0 + 64 * wn + 32 * j + 8 * q + 4 * half;
+        if (n < g.N)
+          st8(crow + n, u32x2{pack_bf16(acc[j][i][4 * q], acc[j][i][4 * q + 1]),
+                              pack_bf16(acc[j][i][4 * q + 2], acc[j][i][4 * q + 3])});
+      }
+  }
+}
+
+template __global__ void gemm_nt_kernel<false>(GemmArgs);
+template __global__ void gemm_nt_kernel<true>(GemmArgs);
+
+}  // namespace
+
+hipError_t launch_gemm(const GemmArgs& g, hipStream_t stream) {
+  const dim3 grid((unsigned)(g.tiles_m * g.tiles_n));
+  if (g.K % kTK != 0)
+    hipLaunchKernelGGL((gemm_nt_kernel<true>), grid, dim3(kThreads), 0, stream, g);
+  else
+    hipLaunchKernelGGL((gemm_nt_kernel<false>), grid, dim3(kThreads), 0, stream, g);
+  return hipGetLastError();
+}
+
+}  // namespace attn

@@ -222,6 +222,30 @@ def make_paged_inputs(w: PagedWorkload, seed: int = 0,
     return PagedInputs(w, q, kc, vc, qo, kv, pages)
 
 
+# ---------------------------------------------------------------------------
+# BF16 GEMM C = A B^T (the paper's fifth primary workload)
+# ---------------------------------------------------------------------------
+
+@dataclass(frozen=True)
+class GemmWorkload:
+    name: str
+    M: int
+    N: int
+    K: int
+
+
+GEMM_WORKLOADS = {
+    "gemm_bf16_nt_m8192_n7168_k5120": GemmWorkload("gemm_bf16_nt_m8192_n7168_k5120",
+                                                   8192, 7168, 5120),
+}
+
+
+def make_gemm_inputs(w: GemmWorkload, seed: int = 0):
+    """A [M, K] then B [N, K], i.i.d. N(0, 1) rounded to bf16."""
+    gen = torch.Generator().manual_seed(seed)
+    return _randn_bf16(gen, (w.M, w.K)), _randn_bf16(gen, (w.N, w.K))
+
+
 def small(name: str, B: int, Hq: int, Hkv: int, S: int, D: int, causal: bool,
           varlen: bool = False, qk_mult: float = 1.0) -> Workload:
     """An ad-hoc workload for shape sweeps (same drawing recipe)."""

@@ -216,3 +216,21 @@ def test_decode_phase_mask_validation():
     args = [A] * 7 + [3, 500, 900, 1000, 24, 8, 128, 0.1, A, 1 << 24]
     for bad in (0, 4, -1):
         assert l.attn_decode_paged_phases(*args, bad, None) == -8
+
+
+def test_gemm_validation():
+    l = attn.lib()
+    g = lambda a=A, b=A, c=A, M=64, N=64, K=64: l.attn_gemm_bf16_nt(a, b, c, M, N, K, None)
+    assert g(M=-1) == -2
+    assert g(K=12) == -2          # K % 8
+    assert g(N=20) == -2          # N % 8
+    assert g(K=1 << 23) == -2     # 256 rows beyond 31-bit offsets
+    assert g(a=0) == -1
+    assert g(c=A + 8) == -5
+    assert g(M=0, a=0, b=0, c=0) == 0
+    assert g(N=0, a=0, b=0, c=0) == 0
+
+
+def test_gemm_empty_k_allows_null_operands():
+    l = attn.lib()
+    assert l.attn_gemm_bf16_nt(A, A, 0, 64, 64, 0, None) == -1   # c is still needed

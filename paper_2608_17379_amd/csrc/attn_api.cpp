@@ -354,7 +354,12 @@ int attn_gemm_bf16_nt(const void* a, const void* b, void* c, int M, int N, int K
   g.K = K;
   g.tiles_m = (M + 255) / 256;
   g.tiles_n = (N + 255) / 256;
-  return attn::launch_gemm(g, stream) == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
+  g.tile0 = 0;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return ATTN_ERR_HIP;
+  return attn::launch_gemm(g, cus, stream) == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
 }
 
 const char* attn_status_string(int status) {

@@ -91,10 +91,12 @@ struct GemmArgs {
   uint16_t* c;
   int M, N, K;
   int tiles_m, tiles_n;
+  int tile0;               // first tile of a launch (set by the launcher)
 };
 
 // Launchers: enqueue on `stream`, return the hipGetLastError() of the launch.
-hipError_t launch_gemm(const GemmArgs& g, hipStream_t stream);
+// cus: compute units of the device (sizes the rounds of workgroups).
+hipError_t launch_gemm(const GemmArgs& g, int cus, hipStream_t stream);
 hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream);
 // Keys per chunk of the decode split (sizes the workspace).
 constexpr int kDecodeChunk = 64;

@@ -13,6 +13,11 @@
 // that each lane holds four consecutive columns of one row of C and stores
 // them as 8 bytes.
 //
+// With one workgroup per CU the tiles run in rounds of one per CU; when the
+// last round would be at most half full, its tiles are computed as 128-row
+// halves by a second launch (8 wavefronts of 64 x 64 each), which fills the
+// chip for half a round instead of half the chip for a whole one.
+//
 // Tiles are assigned XCD by XCD: the hardware hands workgroup ids to the 8
 // XCDs in turn, so workgroup b runs on XCD b % 8; the tiles are numbered so
 // that each XCD receives a contiguous range, walked in bands of 4 row tiles
@@ -38,11 +43,17 @@ static_assert(GTile::NJ == 1, "one DMA instruction per wavefront per 64-row sub-
 constexpr int kSubElems = GTile::ELEMS;            // 4096 bf16
 constexpr int kTileElems = 4 * kSubElems;          // 256 rows
 
-template <bool KTAIL>
+// TM = 256: workgroup b computes tile g.tile0 + b (in the order below).
+// TM = 128: workgroups 2 i and 2 i + 1 compute the two 128-row halves of
+// tile g.tile0 + i.
+template <int TM, bool KTAIL>
 __global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs g) {
-  __shared__ __attribute__((aligned(1024))) uint16_t sa0[kTileElems];
+  constexpr int ASUB = TM / 64;   // 64-row sub-tiles of the A tile
+  constexpr int MB = TM / 64;     // 32-row blocks of each wavefront (4 or 2)
+  constexpr int NB = 2;           // 32-column blocks of each wavefront
+  __shared__ __attribute__((aligned(1024))) uint16_t sa0[ASUB * kSubElems];
   __shared__ __attribute__((aligned(1024))) uint16_t sb0[kTileElems];
-  __shared__ __attribute__((aligned(1024))) uint16_t sa1[kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sa1[ASUB * kSubElems];
   __shared__ __attribute__((aligned(1024))) uint16_t sb1[kTileElems];
 
   const int lane = threadIdx.x & 63, wave = wave_id();
@@ -50,12 +61,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs g) {
 
   // Tile of this workgroup.
   const int nblk = (int)gridDim.x, bid = (int)blockIdx.x;
-  const int t = nblk % 8 == 0 ? (bid % 8) * (nblk / 8) + bid / 8 : bid;
+  const int w = nblk % 8 == 0 ? (bid % 8) * (nblk / 8) + bid / 8 : bid;
+  const int t = g.tile0 + (TM == kTM ? w : w / 2);
   const int band_tiles = kBand * g.tiles_n;
   const int m_first = (t / band_tiles) * kBand;
   const int band_rows = min(kBand, g.tiles_m - m_first);
   const int tb = t % band_tiles;
-  const int m0 = (m_first + tb % band_rows) * kTM;
+  const int m0 = (m_first + tb % band_rows) * kTM + (TM == kTM ? 0 : (w % 2) * TM);
   const int n0 = (tb / band_rows) * kTN;
 
   const int K = g.K;
@@ -75,37 +87,38 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs g) {
     for (int s = 0; s < 4; ++s) {
       int off = doff + 64 * s * row_bytes + 2 * k0;
       if constexpr (KTAIL) off = k0 + 8 * lg < K ? off : kPadOffset;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          ra, (ATTN_LDS void*)(da + s * kSubElems + wave * 64 * 8), 16, off, 0, 0, 0);
+      if (s < ASUB)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            ra, (ATTN_LDS void*)(da + s * kSubElems + wave * 64 * 8), 16, off, 0, 0, 0);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           rb, (ATTN_LDS void*)(db + s * kSubElems + wave * 64 * 8), 16, off, 0, 0, 0);
     }
   };
 
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave >> 2, wn = wave & 3;   // rows (TM / 2) wm .., columns 64 wn ..
   const RowReader<64> rr(l32, half);
   // 32-row block q of a 256-row tile starts at element q * 2048 (sub-tile
   // q / 2, row 32 (q % 2)); the swizzle depends on the row modulo 16 only.
-  f32x16 acc[2][4];
+  f32x16 acc[NB][MB];
 #pragma unroll
-  for (int j = 0; j < 2; ++j)
+  for (int j = 0; j < NB; ++j)
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MB; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
 
   auto compute = [&](const uint16_t* sa, const uint16_t* sb) __attribute__((always_inline)) {
 #pragma unroll
     for (int c = 0; c < kTK / 16; ++c) {
-      u32x4 bo[2], ao[4];
+      u32x4 bo[NB], ao[MB];
 #pragma unroll
-      for (int j = 0; j < 2; ++j) bo[j] = ld16(sb + (2 * wn + j) * 2048 + rr.rm[c]);
+      for (int j = 0; j < NB; ++j) bo[j] = ld16(sb + (NB * wn + j) * 2048 + rr.rm[c]);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) ao[i] = ld16(sa + (4 * wm + i) * 2048 + rr.rm[c]);
+      for (int i = 0; i < MB; ++i) ao[i] = ld16(sa + (MB * wm + i) * 2048 + rr.rm[c]);
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < NB; ++j)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[j][i] = mfma32(bo[j], ao[i], acc[j][i]);
+        for (int i = 0; i < MB; ++i) acc[j][i] = mfma32(bo[j], ao[i], acc[j][i]);
     }
   };
 
@@ -129,14 +142,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs g) {
   if (kt < nkt) step(kt, sa0, sb0, sa1, sb1);
 
   // acc[j][i] is the C^T block of columns n0 + 64 wn + 32 j + (8 (r/4) +
-  // 4 half + r%4) and row m0 + 128 wm + 32 i + l32.
+  // 4 half + r%4) and row m0 + (TM / 2) wm + 32 i + l32.
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int m = m0 + 128 * wm + 32 * i + l32;
+  for (int i = 0; i < MB; ++i) {
+    const int m = m0 + (TM / 2) * wm + 32 * i + l32;
     if (m >= g.M) continue;
     uint16_t* crow = g.c + (int64_t)m * g.N;
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < NB; ++j)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int n = n0 + 64 * wn + 32 * j + 8 * q + 4 * half;
@@ -147,17 +160,40 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs g) {
   }
 }
 
-template __global__ void gemm_nt_kernel<false>(GemmArgs);
-template __global__ void gemm_nt_kernel<true>(GemmArgs);
+template __global__ void gemm_nt_kernel<256, false>(GemmArgs);
+template __global__ void gemm_nt_kernel<256, true>(GemmArgs);
+template __global__ void gemm_nt_kernel<128, false>(GemmArgs);
+template __global__ void gemm_nt_kernel<128, true>(GemmArgs);
+
+template <int TM>
+void launch_part(const GemmArgs& g, int nwg, hipStream_t stream) {
+  if (nwg <= 0) return;
+  if (g.K % kTK != 0)
+    hipLaunchKernelGGL((gemm_nt_kernel<TM, true>), dim3((unsigned)nwg), dim3(kThreads), 0,
+                       stream, g);
+  else
+    hipLaunchKernelGGL((gemm_nt_kernel<TM, false>), dim3((unsigned)nwg), dim3(kThreads), 0,
+                       stream, g);
+}
 
 }  // namespace
 
-hipError_t launch_gemm(const GemmArgs& g, hipStream_t stream) {
-  const dim3 grid((unsigned)(g.tiles_m * g.tiles_n));
-  if (g.K % kTK != 0)
-    hipLaunchKernelGGL((gemm_nt_kernel<true>), grid, dim3(kThreads), 0, stream, g);
-  else
-    hipLaunchKernelGGL((gemm_nt_kernel<false>), grid, dim3(kThreads), 0, stream, g);
+// One workgroup per CU runs at a time, so the tiles go in rounds of `cus`.
+// When the last round would be at most half full, its tiles are split into
+// 128-row halves in a second launch: twice as many workgroups, each half as
+// long, so the last round takes half the time of a full one.
+hipError_t launch_gemm(const GemmArgs& g, int cus, hipStream_t stream) {
+  const int tiles = g.tiles_m * g.tiles_n;
+  const int rem = cus > 0 ? tiles % cus : 0;
+  const bool split = tiles > cus && rem > 0 && 2 * rem <= cus;
+  GemmArgs full = g;
+  full.tile0 = 0;
+  launch_part<kTM>(full, split ? tiles - rem : tiles, stream);
+  if (split) {
+    GemmArgs part = g;
+    part.tile0 = tiles - rem;
+    launch_part<128>(part, 2 * rem, stream);
+  }
   return hipGetLastError();
 }
 

@@ -57,7 +57,10 @@ def _draw(seed, M, N, K):
 
 @pytest.mark.parametrize("M,N,K", [(1, 8, 8), (256, 256, 64), (255, 264, 72), (300, 520, 200),
                                    (513, 1000, 1024), (64, 2048, 136), (1024, 256, 5120),
-                                   (2048, 2048, 512)])
+                                   (2048, 2048, 512),
+                                   # more tiles than CUs with a small last round: that
+                                   # round runs as 128-row half tiles (ragged M, K tail)
+                                   (4252, 4096, 136)])
 def test_gemm_shapes(M, N, K):
     a, b = _draw(M + N + K, M, N, K)
     announce(f"gemm M={M} N={N} K={K}")

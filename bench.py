@@ -16,7 +16,9 @@ batch of seeded synthetic bf16 inputs already resident in HBM.  W untimed
 steps, then K timed steps between two synchronisations; one JSON line is
 printed.  Before the timed steps the GPU runs a spin kernel long enough for
 the host to enqueue all K steps, so the steps run back to back and the
-timing is the GPU's, not the host's launch rate.
+timing is the GPU's, not the host's launch rate.  The K timed steps carry no
+events inside them; a second pass of K steps, not part of `value`, records
+an event around every launch for the per-kernel times.
 
 FLOP convention: forward 4*B*Hq*S^2*D (halved when causal; packed input sums
 L^2 over sequences), backward 2.5x forward.  TFLOP/s = (forward + backward
@@ -25,7 +27,7 @@ x 4096 FLOP/clock/CU).
 
 The roofline object is for the kernel with the largest average duration.
 Each kernel's average duration comes from HIP events recorded between the
-launches inside the timed steps (all on the stream the library launches on).
+launches of the second pass (all on the stream the library launches on).
 Per-launch algorithmic FLOP of each kernel:
   fwd_kernel       2 GEMMs  (S = QK^T, O = PV)            = F
   bwd_dq_kernel    3 GEMMs  (S, dP = dO V^T, dQ = dS K)   = 1.5 F
@@ -154,6 +156,39 @@ def hold_gpu_for_enqueue(host_ms_per_step: float, steps: int) -> None:
     torch.cuda._sleep(int(cycles_per_ms * want_ms))
 
 
+def time_steps(step, n_kernels: int, steps: int, warmup: int):
+    """Run `warmup` steps, then two timed passes of `steps` steps, each after
+    the GPU has been held while the host enqueues it: the first has no events
+    inside the steps (its time per step is the reported one), the second
+    records an event around every launch (per-kernel times).  `step(ev)`
+    records ev[0] before its first launch and ev[1 + i] after launch i.
+    Returns (ms per step, [ms per launch i])."""
+    import torch
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_kernels + 1)]
+           for _ in range(max(steps, warmup, 1))]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(warmup):
+        step(evs[i])
+    host_ms = (time.perf_counter() - t0) * 1e3 / max(1, warmup)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    hold_gpu_for_enqueue(host_ms, steps)
+    start.record()
+    for _ in range(steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(end) / steps
+    hold_gpu_for_enqueue(host_ms, steps)
+    for i in range(steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    kern = [sum(e[j].elapsed_time(e[j + 1]) for e in evs[:steps]) / steps
+            for j in range(n_kernels)]
+    return ms_step, kern
+
+
 # ---------------------------------------------------------------------------
 # Paged key/value cache workloads (forward only, as in the paper)
 # ---------------------------------------------------------------------------
@@ -242,23 +277,8 @@ def run_paged(args, w) -> int:
             if ev is not None:
                 ev[1 + i].record()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(kernels) + 1)]
-           for _ in range(max(args.steps, args.warmup))]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.warmup):
-        step(evs[i])
-    host_ms = (time.perf_counter() - t0) * 1e3 / max(1, args.warmup)
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    hold_gpu_for_enqueue(host_ms, args.steps)
-    start.record()
-    for i in range(args.steps):
-        step(evs[i])
-    end.record()
-    torch.cuda.synchronize()
-    ms_step = start.elapsed_time(end) / args.steps
-    kern_ms = {n: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps
-               for j, n in enumerate(kernels)}
+    ms_step, kl = time_steps(step, len(kernels), args.steps, args.warmup)
+    kern_ms = dict(zip(kernels, kl))
     if not (torch.isfinite(o.float()).all() and torch.isfinite(lse).all()):
         print("non-finite output", file=sys.stderr)
         return 1
@@ -330,22 +350,7 @@ def run_gemm(args, w) -> int:
             ev[1].record()
 
     attn.attn_gemm_bf16_nt(a, b, c)   # shape and pointer checks once, through the binding
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)]
-           for _ in range(max(args.steps, args.warmup))]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.warmup):
-        step(evs[i])
-    host_ms = (time.perf_counter() - t0) * 1e3 / max(1, args.warmup)
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    hold_gpu_for_enqueue(host_ms, args.steps)
-    start.record()
-    for i in range(args.steps):
-        step(evs[i])
-    end.record()
-    torch.cuda.synchronize()
-    ms_step = start.elapsed_time(end) / args.steps
-    kern_ms = sum(e[0].elapsed_time(e[1]) for e in evs[:args.steps]) / args.steps
+    ms_step, (kern_ms,) = time_steps(step, 1, args.steps, args.warmup)
     if not torch.isfinite(c.float()).all():
         print("non-finite output", file=sys.stderr)
         return 1
@@ -461,25 +466,8 @@ def main(argv=None) -> int:
             if ev is not None:
                 ev[2 + i].record()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)]
-           for _ in range(max(args.steps, args.warmup))]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.warmup):
-        step(evs[i])
-    host_ms = (time.perf_counter() - t0) * 1e3 / max(1, args.warmup)
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    hold_gpu_for_enqueue(host_ms, args.steps)
-    start.record()
-    for i in range(args.steps):
-        step(evs[i])
-    end.record()
-    torch.cuda.synchronize()
-    ms_step = start.elapsed_time(end) / args.steps
-    kern_ms = {
-        name: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps
-        for j, name in enumerate(KERNELS)
-    }
+    ms_step, kl = time_steps(step, len(KERNELS), args.steps, args.warmup)
+    kern_ms = dict(zip(KERNELS, kl))
     for t in (o, lse, dq, dk, dv):
         if not torch.isfinite(t.float()).all():
             print("non-finite output", file=sys.stderr)

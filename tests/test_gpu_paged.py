@@ -88,8 +88,8 @@ def _decode(q, kc, vc, kv, idx, max_kvlen, scale, label):
 @pytest.mark.parametrize("Hq,Hkv", [(4, 4), (24, 8), (32, 4), (32, 1)])
 def test_paged_decode(D, Hq, Hkv):
     # one key, one chunk (64 keys) and its neighbours, two chunks and their
-    # neighbours, many chunks, no keys
-    kv_lens = [1, 63, 64, 65, 127, 128, 129, 700, 0, 256]
+    # neighbours, many chunks (up to 19), no keys
+    kv_lens = [1, 63, 64, 65, 127, 128, 129, 700, 0, 256, 1200]
     q, kc, vc, _, kv, idx = _draw(2, [1] * len(kv_lens), kv_lens, Hq, Hkv, D, 4000)
     announce(f"paged decode D={D} Hq={Hq} Hkv={Hkv}")
     _decode(q, kc, vc, kv, idx, max(kv_lens), D ** -0.5, f"decode d{D} g{Hq // Hkv}")

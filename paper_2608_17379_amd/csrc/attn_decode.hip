@@ -176,46 +176,79 @@ __global__ __launch_bounds__(64) void decode_split_kernel(DecodeArgs a) {
   }
 }
 
-// One wavefront per (request, query head).  The chunks' log-sum-exps are
-// read one per lane (64 chunks at a time) and reduced across the wavefront;
-// then lane group gq = lane / CW takes chunks gq, gq + NG, ... and lane
-// l % CW output columns 4 (l % CW) .. + 3 (lanes past column D idle), and
-// the groups' sums are added with cross-lane exchanges.
+// One wavefront per (request, query head).  Lane group gq = lane / CW takes
+// chunks gq, gq + NG, ... and lane l % CW output columns 4 (l % CW) .. + 3
+// (lanes past column D idle); the groups' sums are added with cross-lane
+// exchanges.  The first BATCH chunks' partial outputs and the first 64
+// log-sum-exps (one per lane) are loaded before the request's length is
+// known: they lie inside the workspace rows of this (request, head), and the
+// slots past the request's chunks, which hold stale values, are discarded by
+// selects.  So a request of up to BATCH chunks costs one memory round trip.
 template <int D>
 __global__ __launch_bounds__(64) void decode_merge_kernel(DecodeArgs a) {
   constexpr int CW = D / 4 <= 16 ? 16 : 32;   // lanes per output row (a power of two)
   constexpr int NG = 64 / CW;                 // lane groups
+  constexpr int U = 16;                       // chunks per lane group and batch
+  constexpr int BATCH = NG * U;               // 32 or 64 chunks
+  static_assert(BATCH <= 64, "first-batch weights come from one lane each");
   const int lane = threadIdx.x;
   const int z = blockIdx.x / a.Hq, h = blockIdx.x % a.Hq;
+  const int gq = lane / CW, d = 4 * (lane % CW);
+  const bool col = d < D;
+  const int nck = a.nchunk;
+  const int64_t slot0 = ((int64_t)z * a.Hq + h) * nck;
+  const float* const po = a.part_o + slot0 * D + d;
+  const float* const pl = a.part_lse + slot0;
+
+  // Range-checked loads (zero past this (request, head)'s slots or past
+  // column D), with no branch between them.
+  const rsrc_t ro = make_rsrc(a.part_o + slot0 * D, (int64_t)nck * D * 4);
+  const rsrc_t rl = make_rsrc(pl, (int64_t)nck * 4);
+  const int dcol = col ? 4 * d : kPadOffset;
+  f32x4 v[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    v[u] = __builtin_bit_cast(f32x4, bload16(ro, dcol + 4 * D * (gq + NG * u)));
+  const float l0 = lane < nck ? __int_as_float(bload4(rl, 4 * lane)) : -INFINITY;
+
   int ks = a.kv_cu[z], ke = a.kv_cu[z + 1];
   ks = ks < 0 ? 0 : (ks > a.nnz ? a.nnz : ks);
   ke = ke < ks ? ks : (ke > a.nnz ? a.nnz : ke);
   const int len = min(ke - ks, a.max_kvlen);
   const int nch = (len + kDecodeChunk - 1) / kDecodeChunk;
   if (nch == 1) return;   // written by the split kernel
-  const int gq = lane / CW, d = 4 * (lane % CW);
-  const bool col = d < D;
   uint16_t* op = a.o + ((int64_t)z * a.Hq + h) * D + d;
   if (nch == 0) {   // no keys: O = 0, L = -inf
     if (gq == 0 && col) st8(op, u32x2{0u, 0u});
     if (lane == 0) a.lse[(int64_t)h * a.batch + z] = -INFINITY;
     return;
   }
-  const int64_t slot0 = ((int64_t)z * a.Hq + h) * a.nchunk;
-  float M = -INFINITY;
-  for (int c0 = 0; c0 < nch; c0 += 64)
-    if (c0 + lane < nch) M = fmaxf(M, a.part_lse[slot0 + c0 + lane]);
+
+  // M = max over the request's chunks of L_c, then the weights 2^(L_c - M)
+  // (lane c holds chunk c's weight for the first 64 chunks).
+  float M = lane < nch ? l0 : -INFINITY;
+  for (int c0 = 64; c0 < nch; c0 += 64)
+    if (c0 + lane < nch) M = fmaxf(M, pl[c0 + lane]);
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+  const float wl = lane < nch ? fast_exp2(l0 - M) : 0.f;
+  float wsum = wl;
+  for (int c0 = 64; c0 < nch; c0 += 64)
+    if (c0 + lane < nch) wsum += fast_exp2(pl[c0 + lane] - M);
+
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  float wsum = 0.f;
-  for (int c0 = 0; c0 < nch; c0 += 64) {
-    const float wl = c0 + lane < nch ? fast_exp2(a.part_lse[slot0 + c0 + lane] - M) : 0.f;
-    wsum += wl;
-    const int n = min(64, nch - c0);
-    for (int c = gq; c < n; c += NG) {
-      const float w = __shfl(wl, c);
-      if (col) acc += w * *reinterpret_cast<const f32x4*>(a.part_o + (slot0 + c0 + c) * D + d);
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int c = gq + NG * u;
+    const float w = __shfl(wl, c);
+    if (c < nch) acc += w * v[u];
+  }
+  for (int cb = BATCH; cb < nch; cb += BATCH) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = cb + gq + NG * u;
+      if (c < nch && col)
+        acc += fast_exp2(pl[c] - M) * *reinterpret_cast<const f32x4*>(po + (int64_t)c * D);
     }
   }
 #pragma unroll

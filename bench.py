@@ -5,7 +5,9 @@
 
 Without --workload it measures the headline workload (B4 H16 S2048 D128
 causal).  The paged-cache workloads (paged prefill, paged decode) are forward
-only, as in the paper: their step is one attn_fwd_paged call (TFLOP/s) or one
+only, as in the paper: their step is one attn_fwd_paged call (TFLOP/s; a
+prefill too small to fill the chip is split into key chunks, and the call's
+forward and merge kernels are timed together for the roofline) or one
 attn_decode_paged call (its split and merge kernels; HBM GB/s, with the
 roofline against 8 TB/s since decode reads each key and value once).  The
 GEMM workload's step is one attn_gemm_bf16_nt call (2 M N K FLOP).
@@ -59,7 +61,8 @@ PEAK_HBM_GBS = 8000.0
 METRIC = "attention fwd/bwd TFLOP/s + % bf16 MFMA peak, B4 H16 S2048 D128 causal"
 KERNELS = ("fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel")
 GEMMS = {"fwd_kernel": 2, "bwd_dq_kernel": 3, "bwd_dkdv_kernel": 4}
-KERNEL_SOURCES = {"fwd_kernel": "attn_fwd.hip", "bwd_dq_kernel": "attn_bwd.hip",
+KERNEL_SOURCES = {"fwd_kernel": "attn_fwd.hip", "fwd_kernel+fwd_merge_kernel": "attn_fwd.hip",
+                  "bwd_dq_kernel": "attn_bwd.hip",
                   "bwd_dkdv_kernel": "attn_bwd.hip", "decode_split_kernel": "attn_decode.hip",
                   "decode_merge_kernel": "attn_decode.hip", "gemm_nt_kernel": "gemm.hip"}
 
@@ -263,11 +266,14 @@ def run_paged(args, w) -> int:
             attn.attn_decode_paged_phases(q, kc, vc, o, lse, kv, idx, x.max_kvlen, w.scale, ws,
                                           ph, **host)
     else:
-        kernels = ("fwd_kernel",)
+        # A prefill too small to fill the chip runs split (two kernels in one
+        # call, timed together).
+        ws = attn.prefill_workspace_for(q, kc, w.batch, x.max_qlen, x.max_kvlen)
+        kernels = ("fwd_kernel+fwd_merge_kernel",) if ws is not None else ("fwd_kernel",)
 
         def launch(i):
-            attn.attn_fwd_paged(q, kc, vc, o, lse, qo, kv, idx, x.max_qlen, w.causal, w.scale,
-                                **host)
+            attn.attn_fwd_paged(q, kc, vc, o, lse, qo, kv, idx, x.max_qlen, x.max_kvlen,
+                                w.causal, w.scale, ws, **host)
 
     def step(ev=None):
         if ev is not None:
@@ -307,14 +313,15 @@ def run_paged(args, w) -> int:
                                  "traffic": load_traffic(dom, w.name)}})
         unit_of = lambda n, dt: (total * n / dt / 1e9, "GB/s")
     else:
-        ach = F / (kern_ms["fwd_kernel"] * 1e-3) / 1e12
+        kn = kernels[0]
+        ach = F / (kern_ms[kn] * 1e-3) / 1e12
         rec.update({"metric": f"attention fwd TFLOP/s, {w.name}",
                     "value": round(F / (ms_step * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
                     "pct_peak": round(100 * F / (ms_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
-                    "roofline": {"kernel": "fwd_kernel", "bound": "mfma", "achieved": round(ach, 2),
+                    "roofline": {"kernel": kn, "bound": "mfma", "achieved": round(ach, 2),
                                  "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                                  "frac": round(ach / PEAK_BF16_TFLOPS, 4),
-                                 "traffic": load_traffic("fwd_kernel", w.name)}})
+                                 "traffic": load_traffic(kn, w.name)}})
         unit_of = lambda n, dt: (F * n / dt / 1e12, "TFLOP/s")
     rec["cpu_baseline"] = None if args.no_cpu_baseline else \
         cpu_baseline_paged(x, args.cpu_seconds, unit_of)

@@ -25,7 +25,8 @@ STATUS_NAMES = {
 }
 EXPORTS = ("attn_fwd", "attn_bwd", "attn_bwd_workspace_size", "attn_fwd_varlen",
            "attn_bwd_varlen", "attn_bwd_varlen_workspace_size", "attn_bwd_phases",
-           "attn_bwd_varlen_phases", "attn_fwd_paged", "attn_decode_paged_workspace_size",
+           "attn_bwd_varlen_phases", "attn_fwd_paged_workspace_size", "attn_fwd_paged",
+           "attn_decode_paged_workspace_size",
            "attn_decode_paged", "attn_decode_paged_phases", "attn_gemm_bf16_nt",
            "attn_status_string")
 ATTN_BWD_DQ = 1
@@ -67,7 +68,9 @@ def lib() -> ctypes.CDLL:
         l.attn_bwd_phases.restype = _I
         l.attn_bwd_varlen_phases.argtypes = [_P] * 10 + [_I] * 7 + [_F, _P, _Z, _I, _P]
         l.attn_bwd_varlen_phases.restype = _I
-        l.attn_fwd_paged.argtypes = [_P] * 8 + [_I] * 9 + [_F, _P]
+        l.attn_fwd_paged_workspace_size.argtypes = [_I] * 7
+        l.attn_fwd_paged_workspace_size.restype = _Z
+        l.attn_fwd_paged.argtypes = [_P] * 8 + [_I] * 10 + [_F, _P, _Z, _P]
         l.attn_fwd_paged.restype = _I
         l.attn_decode_paged_workspace_size.argtypes = [_I] * 5
         l.attn_decode_paged_workspace_size.restype = _Z
@@ -269,14 +272,21 @@ def check_paged_host(kv_host: Sequence[int], idx_host: Sequence[int], num_pages:
         raise ValueError("a request has more than max_kvlen keys")
 
 
+def attn_fwd_paged_workspace_size(batch: int, max_qlen: int, total_q: int, max_kvlen: int,
+                                  Hq: int, Hkv: int, D: int) -> int:
+    return int(lib().attn_fwd_paged_workspace_size(batch, max_qlen, total_q, max_kvlen, Hq,
+                                                   Hkv, D))
+
+
 def attn_fwd_paged(q, k_cache, v_cache, o, lse, qo_indptr, kv_indptr, kv_indices,
-                   max_qlen: int, causal: bool, scale: float, stream=None,
-                   qo_indptr_host=None, kv_indptr_host=None, kv_indices_host=None,
+                   max_qlen: int, max_kvlen: int, causal: bool, scale: float, workspace=None,
+                   stream=None, qo_indptr_host=None, kv_indptr_host=None, kv_indices_host=None,
                    checked: bool = False) -> None:
     """Paged prefill.  The index arrays are checked on the host (from the
     *_host copies when given, else from a device-to-host copy) unless
     `checked` says the caller has already done so with check_cu_seqlens and
-    check_paged_host for these arrays."""
+    check_paged_host for these arrays.  `workspace` None runs the prefill
+    unsplit (see attn_fwd_paged_workspace_size)."""
     Tq, Hq, D = q.shape
     P, Hkv = k_cache.shape[0], k_cache.shape[1]
     _shape(k_cache, (P, Hkv, D), "k_cache")
@@ -289,15 +299,18 @@ def attn_fwd_paged(q, k_cache, v_cache, o, lse, qo_indptr, kv_indptr, kv_indices
     if not checked:
         check_cu_seqlens(_host_list(qo_indptr, qo_indptr_host), Tq, max_qlen)
         check_paged_host(_host_list(kv_indptr, kv_indptr_host),
-                         _host_list(kv_indices, kv_indices_host), P)
+                         _host_list(kv_indices, kv_indices_host), P, max_kvlen)
     nnz = kv_indices.numel()
     st = lib().attn_fwd_paged(_ptr(q, "q"), _ptr(k_cache, "k_cache"), _ptr(v_cache, "v_cache"),
                               _ptr(o, "o"), _ptr(lse, "lse", torch.float32),
                               _ptr(qo_indptr, "qo_indptr", torch.int32),
                               _ptr(kv_indptr, "kv_indptr", torch.int32),
                               _ptr(kv_indices, "kv_indices", torch.int32) if nnz else 0,
-                              batch, int(max_qlen), Tq, nnz, P, Hq, Hkv, D, int(bool(causal)),
-                              float(scale), _stream(stream))
+                              batch, int(max_qlen), Tq, int(max_kvlen), nnz, P, Hq, Hkv, D,
+                              int(bool(causal)), float(scale),
+                              _ptr(workspace, "workspace", torch.uint8) if workspace is not None
+                              else 0,
+                              workspace.numel() if workspace is not None else 0, _stream(stream))
     _check(st, "attn_fwd_paged")
 
 
@@ -363,13 +376,29 @@ def gemm_nt(a, b):
 # Allocating conveniences (torch allocates the outputs; the library fills them)
 # --------------------------------------------------------------------------
 
+def prefill_workspace_for(q, k_cache, batch: int, max_qlen: int, max_kvlen: int):
+    """The workspace attn_fwd_paged needs for these shapes, or None when it
+    runs unsplit."""
+    Tq, Hq, D = q.shape
+    n = attn_fwd_paged_workspace_size(batch, max_qlen, Tq, max_kvlen, Hq, k_cache.shape[1], D)
+    return torch.empty(n, dtype=torch.uint8, device=q.device) if n else None
+
+
 def forward_paged(q, k_cache, v_cache, qo_indptr, kv_indptr, kv_indices, max_qlen: int,
-                  causal: bool, scale: float, **host):
-    """Return (o, lse) of a paged prefill (packed queries)."""
+                  causal: bool, scale: float, max_kvlen: Optional[int] = None,
+                  split: bool = True, **host):
+    """Return (o, lse) of a paged prefill (packed queries).  max_kvlen
+    defaults to the longest request of kv_indptr; split False runs the
+    prefill unsplit."""
+    if max_kvlen is None:
+        kv = _host_list(kv_indptr, host.get("kv_indptr_host"))
+        max_kvlen = max((b - a for a, b in zip(kv, kv[1:])), default=0)
     o = torch.empty_like(q)
     lse = torch.empty((q.shape[1], q.shape[0]), dtype=torch.float32, device=q.device)
+    ws = (prefill_workspace_for(q, k_cache, qo_indptr.numel() - 1, max_qlen, max_kvlen)
+          if split else None)
     attn_fwd_paged(q, k_cache, v_cache, o, lse, qo_indptr, kv_indptr, kv_indices, max_qlen,
-                   causal, scale, **host)
+                   max_kvlen, causal, scale, ws, **host)
     return o, lse
 
 

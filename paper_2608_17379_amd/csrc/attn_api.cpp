@@ -88,11 +88,28 @@ bool any_misaligned(std::initializer_list<const void*> ps) {
   return false;
 }
 
+// Key split of a paged prefill (see attn::FwdArgs).
+struct PagedSplit {
+  int max_kvlen;
+  int split;
+  int nsplit;
+  float* part_o;
+  float* part_lse;
+};
+
 int fwd_common(const void* q, const void* k, const void* v, void* o, float* lse,
-               const Layout& L, int D, int causal, float scale, hipStream_t stream) {
+               const Layout& L, int D, int causal, float scale, hipStream_t stream,
+               const PagedSplit* ps = nullptr) {
   if (any_null({q, k, v, o, lse})) return ATTN_ERR_NULL;
   if (any_misaligned({q, k, v, o, lse})) return ATTN_ERR_ALIGN;
-  attn::FwdArgs a;
+  attn::FwdArgs a{};
+  if (ps) {
+    a.max_kvlen = ps->max_kvlen;
+    a.split = ps->split;
+    a.nsplit = ps->nsplit;
+    a.part_o = ps->part_o;
+    a.part_lse = ps->part_lse;
+  }
   a.L = L;
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);
@@ -147,6 +164,20 @@ int64_t decode_chunks(int max_kvlen) {
 }
 
 size_t round256(int64_t bytes) { return (size_t)((bytes + 255) / 256 * 256); }
+
+// A paged prefill whose unsplit grid (a workgroup per query block and its
+// causal mirror, per request and query head) has fewer workgroups than the
+// MI355X has CUs is split into chunks of keys, when its requests are longer
+// than one chunk.  The rule uses the part's CU count, not a device query, so
+// that the workspace size depends on the shapes alone.
+constexpr int kChipCUs = 256;
+
+int paged_split(int batch, int max_qlen, int max_kvlen, int Hq) {
+  const int64_t nqt = ((int64_t)max_qlen + attn::kFwdBlockRows - 1) / attn::kFwdBlockRows;
+  const int64_t wgs = (int64_t)batch * Hq * ((nqt + 1) / 2);
+  if (max_kvlen <= attn::kFwdSplitKeys || wgs >= kChipCUs) return 0;
+  return attn::kFwdSplitKeys;
+}
 
 size_t delta_bytes(int64_t rows_times_heads) {
   // fp32 Delta and fp32 L log2(e) per (row, query head), each array rounded
@@ -249,13 +280,26 @@ int attn_bwd_varlen(const void* q, const void* k, const void* v, const void* o, 
                                 ATTN_BWD_DQ | ATTN_BWD_DKDV, stream);
 }
 
+size_t attn_fwd_paged_workspace_size(int batch, int max_qlen, int total_q, int max_kvlen,
+                                     int Hq, int Hkv, int D) {
+  (void)Hkv;
+  if (batch <= 0 || max_qlen <= 0 || total_q <= 0 || max_kvlen <= 0 || Hq <= 0 || D <= 0)
+    return 0;
+  const int split = paged_split(batch, max_qlen, max_kvlen, Hq);
+  if (split == 0) return 0;
+  const int64_t slots = (int64_t)total_q * Hq * ((max_kvlen + split - 1) / split);
+  return round256(slots * D * 4) + round256(slots * 4);
+}
+
 int attn_fwd_paged(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse,
                    const int* qo_indptr, const int* kv_indptr, const int* kv_indices, int batch,
-                   int max_qlen, int total_q, int nnz, int num_pages, int Hq, int Hkv, int D,
-                   int causal, float scale, hipStream_t stream) {
+                   int max_qlen, int total_q, int max_kvlen, int nnz, int num_pages, int Hq,
+                   int Hkv, int D, int causal, float scale, void* workspace,
+                   size_t workspace_bytes, hipStream_t stream) {
   int st = check_common(Hq, Hkv, D, causal, scale);
   if (st != ATTN_OK) return st;
   if (batch < 0 || total_q < 0 || check_rows(max_qlen) != ATTN_OK) return ATTN_ERR_SHAPE;
+  if (check_rows(max_kvlen) != ATTN_OK) return ATTN_ERR_SHAPE;
   if ((st = check_cache(num_pages, nnz, Hkv, D)) != ATTN_OK) return st;
   if ((int64_t)batch * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
   if (batch == 0 || total_q == 0) return ATTN_OK;
@@ -263,13 +307,28 @@ int attn_fwd_paged(const void* q, const void* k_cache, const void* v_cache, void
   if (!qo_indptr || !kv_indptr || (nnz > 0 && !kv_indices)) return ATTN_ERR_NULL;
   if (misaligned4(qo_indptr) || misaligned4(kv_indptr) || misaligned4(kv_indices))
     return ATTN_ERR_ALIGN;
+  if (any_null({q, k_cache, v_cache, o, lse})) return ATTN_ERR_NULL;
+  if (any_misaligned({q, k_cache, v_cache, o, lse})) return ATTN_ERR_ALIGN;
   Layout L = packed_layout(qo_indptr, batch, max_qlen, total_q, Hq, Hkv, D);
   // The cache [num_pages, Hkv, D] has the packed key layout with a page per row.
   L.kv_cu = kv_indptr;
   L.kv_idx = kv_indices;
   L.nnz = nnz;
   L.num_pages = num_pages;
-  return fwd_common(q, k_cache, v_cache, o, lse, L, D, causal, scale, stream);
+  // Without a workspace the forward runs unsplit.
+  int split = workspace ? paged_split(batch, max_qlen, max_kvlen, Hq) : 0;
+  PagedSplit ps{max_kvlen, split, 0, nullptr, nullptr};
+  if (split > 0) {
+    const size_t need = attn_fwd_paged_workspace_size(batch, max_qlen, total_q, max_kvlen, Hq,
+                                                      Hkv, D);
+    if (workspace_bytes < need) return ATTN_ERR_WORKSPACE;
+    if (misaligned(workspace)) return ATTN_ERR_ALIGN;
+    ps.nsplit = (max_kvlen + split - 1) / split;
+    const int64_t slots = (int64_t)total_q * Hq * ps.nsplit;
+    ps.part_o = static_cast<float*>(workspace);
+    ps.part_lse = reinterpret_cast<float*>(static_cast<char*>(workspace) + round256(slots * D * 4));
+  }
+  return fwd_common(q, k_cache, v_cache, o, lse, L, D, causal, scale, stream, &ps);
 }
 
 size_t attn_decode_paged_workspace_size(int batch, int max_kvlen, int Hq, int Hkv, int D) {

@@ -34,7 +34,8 @@ namespace attn {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kBM = 128;   // query rows per workgroup
+constexpr int kBM = kFwdBlockRows;   // query rows per workgroup
+static_assert(kFwdSplitKeys % 128 == 0, "a chunk starts on an even key tile (stage 0)");
 constexpr int kBN = 64;    // keys per iteration
 constexpr float kRescaleSlack = 8.0f;   // log2 of the largest P entry allowed
 
@@ -64,20 +65,23 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   // last seg.len of the kv_len key positions, so query row i sits at key
   // position i + dpos.
   const Segment kseg = PAGED ? kv_segment_of(L, z) : seg;
-  const int kv_len = kseg.len;
+  const int kv_len = PAGED ? min(kseg.len, a.max_kvlen) : kseg.len;
   const int dpos = PAGED ? kv_len - seg.len : 0;
-  // Query blocks nqt - 1 - p and p of the segment, in that order: under the
-  // causal mask every workgroup then has the same number of key tiles, so the
-  // two workgroups sharing a CU finish together.
+  // Unsplit: query blocks nqt - 1 - p and p of the segment, in that order:
+  // under the causal mask every workgroup then has the same number of key
+  // tiles, so the two workgroups sharing a CU finish together.  Split: query
+  // block p, key chunk blockIdx.z.
   const int nqt = (seg.len + kBM - 1) / kBM;
   const int p = (int)blockIdx.y;
-  if (p > nqt - 1 - p) return;
+  const int split = PAGED ? a.split : 0;
+  const int chunk = (int)blockIdx.z;
+  if (split ? p >= nqt : p > nqt - 1 - p) return;
 
 #pragma nounroll
   for (int pass = 0; pass < 2; ++pass) {
-    const int qt = pass == 0 ? nqt - 1 - p : p;
+    const int qt = split ? p : pass == 0 ? nqt - 1 - p : p;
     if (pass == 1) {
-      if (qt >= nqt - 1 - p) break;
+      if (split || qt >= nqt - 1 - p) break;
       __syncthreads();   // the first block's last tile is read before stage 0 refills
     }
     const int q0 = qt * kBM;
@@ -104,6 +108,13 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
 
     const int kend = a.causal ? min(kv_len, max(0, q0 + kBM + dpos)) : kv_len;
     const int nkt = (kend + kBN - 1) / kBN;
+    // This workgroup's key tiles [kt_lo, kt_hi): all of them, or one chunk.
+    // A block with no visible key has one (empty) chunk, which writes the
+    // rows' O = 0 and L = -inf.
+    const int nch = split ? max(1, (kend + split - 1) / split) : 1;
+    if (chunk >= nch) return;   // split only (unsplit grids have one z slice)
+    const int kt_lo = split ? chunk * (split / kBN) : 0;
+    const int kt_hi = split ? min(nkt, kt_lo + split / kBN) : nkt;
 
     const Tile dma(wave, lane, (int)(L.kv_row * 2));
     const RowReader<D> kr(l32, half);
@@ -150,7 +161,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
         }
         dma.load_at(kcache, off, kd, wave);
         dma.load_at(vcache, off, vd, wave);
-        if (kt + 1 < nkt) fetch(kt + 1);
+        if (kt + 1 < kt_hi) fetch(kt + 1);
       } else {
         dma.load(rows_rsrc(kp, kt * kBN, kv_len, kv_row), kd, wave);
         dma.load(rows_rsrc(vp, kt * kBN, kv_len, kv_row), vd, wave);
@@ -232,20 +243,21 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
                     uint16_t* vn) __attribute__((always_inline)) {
       wait_vm<0>();
       __syncthreads();
-      if (kt + 1 < nkt) load_tile(kt + 1, kn, vn);
+      if (kt + 1 < kt_hi) load_tile(kt + 1, kn, vn);
       if (work) compute(kt, kc, vc);
     };
 
     // Tiles past this wavefront's last query are fully masked for it: the
     // wavefront only joins their barriers and loads.
     const int last_key = qw0 + 31 + dpos;   // the wavefront's last visible key (causal)
-    const int nkt_w = causal ? (last_key < 0 ? 0 : min(nkt, last_key / kBN + 1)) : nkt;
-    if (nkt > 0) {
-      if constexpr (PAGED) fetch(0);
-      load_tile(0, sk0, sv0);
+    const int nkt_w = causal ? (last_key < 0 ? 0 : min(kt_hi, last_key / kBN + 1)) : kt_hi;
+    if (kt_hi > kt_lo) {
+      if constexpr (PAGED) fetch(kt_lo);
+      load_tile(kt_lo, sk0, sv0);
     }
     wait_vm<0>();   // Q rows and the first tile
-    int kt = 0;
+    // Tile kt uses stage kt % 2 (kt_lo is even).
+    int kt = kt_lo;
     for (; kt + 1 < nkt_w; kt += 2) {
       step(kt, true, sk0, sv0, sk1, sv1);
       step(kt + 1, true, sk1, sv1, sk0, sv0);
@@ -254,16 +266,32 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
       step(kt, true, sk0, sv0, sk1, sv1);
       ++kt;
     }
-    for (; kt < nkt; ++kt) {
+    for (; kt < kt_hi; ++kt) {
       if (kt & 1)
         step(kt, false, sk1, sv1, sk0, sv0);
       else
         step(kt, false, sk0, sv0, sk1, sv1);
     }
 
-    // Epilogue: O = O / l, L = (m + log2 l) ln 2.
+    // Epilogue: O = O / l, L = (m + log2 l) ln 2; or, for one chunk of
+    // several, the chunk's O / l and m + log2 l (base 2) as a partial result.
     lsum += swap_halves(lsum);
-    if (qrow < seg.len) {
+    if (nch > 1) {
+      if (qrow < seg.len) {
+        const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+        const int64_t slot = ((int64_t)(seg.start + qrow) * L.Hq + h) * a.nsplit + chunk;
+        float* po = a.part_o + slot * D + 4 * half;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+            *reinterpret_cast<f32x4*>(po + 32 * db + 8 * g) =
+                f32x4{oacc[db][4 * g], oacc[db][4 * g + 1], oacc[db][4 * g + 2],
+                      oacc[db][4 * g + 3]} *
+                inv;
+        if (half == 0) a.part_lse[slot] = lsum > 0.f ? mref + log2f(lsum) : -INFINITY;
+      }
+    } else if (qrow < seg.len) {
       const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
       uint16_t* op = a.o + qoff + (int64_t)qrow * L.q_row;
 #pragma unroll
@@ -280,6 +308,93 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   }
 }
 
+// Merge of a split paged prefill: for each query row of a block with more
+// than one key chunk, O = sum_c 2^(L_c - M) O_c / sum_c 2^(L_c - M) and
+// L = (M + log2 sum_c 2^(L_c - M)) ln 2, M = max_c L_c.  A chunk in which the
+// row sees no key has L_c = -inf and weight 0; a row that sees no key at all
+// gets O = 0 and L = -inf.  One workgroup of 4 wavefronts per (segment, query
+// head, 32 rows of a query block); half a wavefront per row, 4 output columns
+// per lane, kMergePasses rows per half wavefront.  Every load of the first
+// kMergeU chunks of all its rows is issued before any is used: the chunk
+// index is clamped into the row's chunks (the loads are always in bounds and
+// need no branch) and the clamped repeats are dropped by selects.
+constexpr int kMergePasses = 4;
+constexpr int kMergeRows = 8 * kMergePasses;
+constexpr int kMergeU = 4;
+
+template <int D>
+__global__ __launch_bounds__(256) void fwd_merge_kernel(FwdArgs a) {
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const Layout L = a.L;
+  const int z = blockIdx.x / L.Hq, h = blockIdx.x % L.Hq;
+  const Segment seg = segment_of(L, z);
+  const int kv_len = min(kv_segment_of(L, z).len, a.max_kvlen);
+  const int dpos = kv_len - seg.len;
+  const int q0 = (int)blockIdx.y * kBM;
+  if (q0 >= seg.len) return;
+  const int kend = a.causal ? min(kv_len, max(0, q0 + kBM + dpos)) : kv_len;
+  const int nch = (kend + a.split - 1) / a.split;
+  if (nch <= 1) return;   // the forward wrote the block's rows itself
+  const int row0 = q0 + (int)blockIdx.z * kMergeRows + 2 * wave + (lane >> 5);
+  const int dl = 4 * (lane & 31);
+  const bool col = dl < D;
+  const int d = col ? dl : 0;
+
+  float l[kMergePasses][kMergeU];
+  f32x4 v[kMergePasses][kMergeU];
+#pragma unroll
+  for (int i = 0; i < kMergePasses; ++i) {
+    const int row = min(row0 + 8 * i, seg.len - 1);
+    const int64_t slot0 = ((int64_t)(seg.start + row) * L.Hq + h) * a.nsplit;
+#pragma unroll
+    for (int u = 0; u < kMergeU; ++u) {
+      const int c = min(u, nch - 1);
+      l[i][u] = a.part_lse[slot0 + c];
+      v[i][u] = *reinterpret_cast<const f32x4*>(a.part_o + (slot0 + c) * D + d);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kMergePasses; ++i) {
+    const int row = row0 + 8 * i;
+    if (row >= seg.len) break;
+    const int64_t slot0 = ((int64_t)(seg.start + row) * L.Hq + h) * a.nsplit;
+    const float* const pl = a.part_lse + slot0;
+    const float* const po = a.part_o + slot0 * D + d;
+    float M = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kMergeU; ++u)
+      if (u < nch) M = fmaxf(M, l[i][u]);
+    for (int c = kMergeU; c < nch; ++c) M = fmaxf(M, pl[c]);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    float wsum = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int u = 0; u < kMergeU; ++u)
+        if (u < nch) {
+          const float w = fast_exp2(l[i][u] - M);
+          wsum += w;
+          acc += w * v[i][u];
+        }
+      for (int c = kMergeU; c < nch; ++c) {
+        const float w = fast_exp2(pl[c] - M);
+        wsum += w;
+        acc += w * *reinterpret_cast<const f32x4*>(po + (int64_t)c * D);
+      }
+    }
+    const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+    if (col)
+      st8(a.o + (int64_t)(seg.start + row) * L.q_row + (int64_t)h * L.q_head + d,
+          u32x2{pack_bf16(acc[0] * inv, acc[1] * inv), pack_bf16(acc[2] * inv, acc[3] * inv)});
+    if ((lane & 31) == 0)
+      a.lse[(int64_t)seg.start + (int64_t)h * L.r_head + row] =
+          wsum > 0.f ? (M + log2f(wsum)) * kLn2 : -INFINITY;
+  }
+}
+
+template __global__ void fwd_merge_kernel<64>(FwdArgs);
+template __global__ void fwd_merge_kernel<96>(FwdArgs);
+template __global__ void fwd_merge_kernel<128>(FwdArgs);
+
 // Explicit instantiations: without them the host compiler may skip the
 // launch stubs of these templates (leaving undefined symbols in the library).
 template __global__ void fwd_kernel<64, false>(FwdArgs);
@@ -288,6 +403,11 @@ template __global__ void fwd_kernel<128, false>(FwdArgs);
 template __global__ void fwd_kernel<64, true>(FwdArgs);
 template __global__ void fwd_kernel<96, true>(FwdArgs);
 template __global__ void fwd_kernel<128, true>(FwdArgs);
+
+template <int D>
+void launch_merge(const FwdArgs& a, dim3 grid, hipStream_t stream) {
+  hipLaunchKernelGGL((fwd_merge_kernel<D>), grid, dim3(256), 0, stream, a);
+}
 
 template <bool PAGED>
 void launch_fwd_p(const FwdArgs& a, int D, dim3 grid, hipStream_t stream) {
@@ -302,9 +422,22 @@ void launch_fwd_p(const FwdArgs& a, int D, dim3 grid, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream) {
-  // Each workgroup takes a query block and its mirror (see the kernel).
   const int nqt = (a.L.S + kBM - 1) / kBM;
-  const dim3 grid((unsigned)(a.L.nseg * a.L.Hq), (unsigned)((nqt + 1) / 2));
+  const unsigned heads = (unsigned)(a.L.nseg * a.L.Hq);
+  if (a.L.kv_cu && a.split > 0) {
+    // One workgroup per (query block, key chunk), then the merge.
+    launch_fwd_p<true>(a, D, dim3(heads, (unsigned)nqt, (unsigned)a.nsplit), stream);
+    const dim3 mg(heads, (unsigned)nqt, (unsigned)(kBM / kMergeRows));
+    if (D == 64)
+      launch_merge<64>(a, mg, stream);
+    else if (D == 96)
+      launch_merge<96>(a, mg, stream);
+    else
+      launch_merge<128>(a, mg, stream);
+    return hipGetLastError();
+  }
+  // Each workgroup takes a query block and its mirror (see the kernel).
+  const dim3 grid(heads, (unsigned)((nqt + 1) / 2));
   if (a.L.kv_cu)
     launch_fwd_p<true>(a, D, grid, stream);
   else

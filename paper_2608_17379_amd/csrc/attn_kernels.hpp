@@ -45,6 +45,16 @@ struct FwdArgs {
   float* lse;
   float scale_log2;        // softmax scale * log2(e)
   int causal;
+  // Paged prefill only.  Keys of a request past max_kvlen are ignored.  With
+  // split > 0 the keys of every query block are cut into chunks of `split`
+  // keys (a multiple of 128), one workgroup each: a block with more than one
+  // chunk writes normalised partial outputs and base-2 log-sum-exps to the
+  // workspace, which fwd_merge_kernel combines.
+  int max_kvlen;
+  int split;               // keys per chunk, or 0 (unsplit)
+  int nsplit;              // chunk slots per (query row, head): the grid's z extent
+  float* part_o;           // workspace [total_q, Hq, nsplit, D] fp32
+  float* part_lse;         // workspace [total_q, Hq, nsplit] fp32, log2 units
 };
 
 struct BwdArgs {
@@ -100,6 +110,8 @@ hipError_t launch_gemm(const GemmArgs& g, int cus, hipStream_t stream);
 hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream);
 // Keys per chunk of the decode split (sizes the workspace).
 constexpr int kDecodeChunk = 64;
+constexpr int kFwdSplitKeys = 256;   // keys per chunk of a split paged prefill
+constexpr int kFwdBlockRows = 128;   // query rows per forward workgroup
 // phases: bit 0 = split kernel, bit 1 = merge kernel.
 hipError_t launch_decode(const DecodeArgs& a, int D, int phases, hipStream_t stream);
 // phases: bit 0 = Delta and dQ kernel, bit 1 = dK/dV kernel.

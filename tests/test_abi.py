@@ -148,12 +148,15 @@ def test_cu_seqlens_host_check():
 
 
 def fwdp(**kw):
-    args = dict(q=A, k=A, v=A, o=A, lse=A, qo=A, kv=A, idx=A, batch=2, mq=64, Tq=100, nnz=120,
-                P=1000, Hq=4, Hkv=2, D=128, causal=1, scale=0.1)
+    # A split-size prefill (8 unsplit workgroups, 600 keys) with a workspace
+    # one byte short, so that no valid combination reaches a launch.
+    args = dict(q=A, k=A, v=A, o=A, lse=A, qo=A, kv=A, idx=A, batch=2, mq=64, Tq=100, mk=600,
+                nnz=120, P=1000, Hq=4, Hkv=2, D=128, causal=1, scale=0.1, ws=A,
+                wsb=attn.attn_fwd_paged_workspace_size(2, 64, 100, 600, 4, 2, 128) - 1)
     args.update(kw)
     return attn.lib().attn_fwd_paged(*(args[n] for n in (
-        "q", "k", "v", "o", "lse", "qo", "kv", "idx", "batch", "mq", "Tq", "nnz", "P", "Hq", "Hkv",
-        "D", "causal", "scale")), None)
+        "q", "k", "v", "o", "lse", "qo", "kv", "idx", "batch", "mq", "Tq", "mk", "nnz", "P", "Hq",
+        "Hkv", "D", "causal", "scale", "ws", "wsb")), None)
 
 
 def dec(**kw):
@@ -188,7 +191,23 @@ def test_paged_prefill_specific_validation():
     assert fwdp(mq=0) == -8
     assert fwdp(qo=0) == -1
     assert fwdp(Tq=-1) == -2
+    assert fwdp(mk=-1) == -2
     assert fwdp(Tq=0, q=0, qo=0) == 0
+    assert fwdp() == -6                                  # workspace one byte short
+    assert fwdp(wsb=1 << 30, ws=A + 8) == -5             # misaligned workspace
+
+
+def test_paged_prefill_workspace_size():
+    size = attn.attn_fwd_paged_workspace_size
+    # split: 2 x 4 x 1 unsplit workgroups, 600 keys -> 3 chunks of 256
+    slots = 100 * 4 * 3
+    assert size(2, 64, 100, 600, 4, 2, 128) == (slots * 128 * 4 + 255) // 256 * 256 + \
+        (slots * 4 + 255) // 256 * 256
+    assert size(2, 64, 100, 256, 4, 2, 128) == 0         # one chunk: no split
+    assert size(64, 4096, 64 * 4096, 4096, 32, 8, 128) == 0   # the grid fills the chip
+    assert size(1, 892, 892, 892, 24, 8, 128) > 0        # the paper's paged prefill
+    assert size(0, 64, 100, 600, 4, 2, 128) == 0
+    assert size(2, 64, 100, 0, 4, 2, 128) == 0
 
 
 def test_decode_specific_validation():

@@ -4,8 +4,12 @@ attn_decode_paged, called through the C ABI by the binding.
 
 Small cases span several key tiles (64 keys forward), several decode chunks
 (64 keys) and ragged tails, with head dimensions 64, 96 and 128, grouped
-query heads, requests with fewer queries than keys, and empty requests.  The
-paper's two paged workloads run at full size, compared on every head.
+query heads, requests with fewer queries than keys, and empty requests.
+Paged prefill runs both ways: split into 256-key chunks with a merge (what
+the library does when the grid is small, as in every case here) and
+unsplit (no workspace); the split cases include blocks of one to four
+chunks and ragged last chunks.  The paper's two paged workloads run at full
+size, compared on every head.
 """
 import pytest
 import torch
@@ -51,27 +55,32 @@ def _check(o, lse, ro, rl, label):
     assert el <= LSE_MAXABS, (label, el)
 
 
-def _prefill(q, kc, vc, qo, kv, idx, causal, scale, label):
+def _prefill(q, kc, vc, qo, kv, idx, causal, scale, label, split=True):
     dq, dkc, dvc = _dev(q, kc, vc)
     o, lse = attn.forward_paged(dq, dkc, dvc, _i32(qo), _i32(kv), _i32(idx),
                                 max(b - a for a, b in zip(qo, qo[1:])), causal, scale,
-                                qo_indptr_host=qo, kv_indptr_host=kv, kv_indices_host=idx)
+                                split=split, qo_indptr_host=qo, kv_indptr_host=kv,
+                                kv_indices_host=idx)
     torch.cuda.synchronize()
     ro, rl = oracle.attention_forward_paged(q, kc, vc, qo, kv, idx, causal, scale)
     _check(o, lse, ro, rl, label)
 
 
+@pytest.mark.parametrize("split", [True, False])
 @pytest.mark.parametrize("D", [64, 96, 128])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("Hq,Hkv", [(2, 2), (6, 2)])
-def test_paged_prefill(D, causal, Hq, Hkv):
+def test_paged_prefill(D, causal, Hq, Hkv, split):
     # q_len == kv_len, q_len < kv_len (a continued prefill), one key, a
-    # request with more queries than keys, an empty request
-    q_lens = [200, 37, 1, 70, 0, 129]
-    kv_lens = [200, 300, 1, 5, 0, 129]
-    args = _draw(1, q_lens, kv_lens, Hq, Hkv, D, 1500)
-    announce(f"paged prefill D={D} causal={causal} Hq={Hq} Hkv={Hkv}")
-    _prefill(*args, causal, D ** -0.5, f"prefill d{D} c{int(causal)} g{Hq // Hkv}")
+    # request with more queries than keys, an empty request, a request of
+    # blocks with one to four 256-key chunks (the last ragged), and one with
+    # more queries than keys over several chunks
+    q_lens = [200, 37, 1, 70, 0, 129, 700, 600]
+    kv_lens = [200, 300, 1, 5, 0, 129, 900, 520]
+    args = _draw(1, q_lens, kv_lens, Hq, Hkv, D, 4000)
+    announce(f"paged prefill D={D} causal={causal} Hq={Hq} Hkv={Hkv} split={split}")
+    _prefill(*args, causal, D ** -0.5, f"prefill d{D} c{int(causal)} g{Hq // Hkv} s{int(split)}",
+             split)
 
 
 def _decode(q, kc, vc, kv, idx, max_kvlen, scale, label):
@@ -125,25 +134,44 @@ def test_decode_workspace_larger_max_kvlen_and_guard_bands():
         assert (b[:pad].float() == sent).all() and (b[-pad:].float() == sent).all()
 
 
-def test_paged_prefill_guard_bands_and_determinism():
-    q, kc, vc, qo, kv, idx = _draw(5, [150, 64], [150, 90], 4, 2, 128, 600)
+@pytest.mark.parametrize("split", [True, False])
+def test_paged_prefill_guard_bands_and_determinism(split):
+    """Nothing is written outside o and lse; two calls give the same bits
+    (split: the second call reuses the first call's workspace)."""
+    q_lens, kv_lens = [150, 64], [600, 90]
+    q, kc, vc, qo, kv, idx = _draw(5, q_lens, kv_lens, 4, 2, 128, 1000)
     dq, dkc, dvc = _dev(q, kc, vc)
+    Tq = sum(q_lens)
     pad, sent = 4096, -1536.0
     ob = torch.full((q.numel() + 2 * pad,), sent, dtype=torch.bfloat16, device="cuda")
-    lb = torch.full((4 * 214 + 2 * pad,), sent, dtype=torch.float32, device="cuda")
+    lb = torch.full((4 * Tq + 2 * pad,), sent, dtype=torch.float32, device="cuda")
     o = ob[pad:pad + q.numel()].view(q.shape)
-    lse = lb[pad:pad + 4 * 214].view(4, 214)
+    lse = lb[pad:pad + 4 * Tq].view(4, Tq)
+    ws = attn.prefill_workspace_for(dq, dkc, 2, 150, 600) if split else None
+    assert (ws is not None) == split   # these shapes are split when a workspace is given
     outs = []
     for _ in range(2):
-        attn.attn_fwd_paged(dq, dkc, dvc, o, lse, _i32(qo), _i32(kv), _i32(idx), 150, True,
-                            128 ** -0.5)
+        attn.attn_fwd_paged(dq, dkc, dvc, o, lse, _i32(qo), _i32(kv), _i32(idx), 150, 600, True,
+                            128 ** -0.5, ws)
         torch.cuda.synchronize()
         outs.append((o.clone(), lse.clone()))
     assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
     ro, rl = oracle.attention_forward_paged(q, kc, vc, qo, kv, idx, True, 128 ** -0.5)
-    _check(o, lse, ro, rl, "prefill guard")
+    _check(o, lse, ro, rl, f"prefill guard split={split}")
     for b in (ob, lb):
         assert (b[:pad].float() == sent).all() and (b[-pad:].float() == sent).all()
+
+
+def test_paged_prefill_max_kvlen_above_every_request():
+    """A larger max_kvlen only adds empty chunks."""
+    q, kc, vc, qo, kv, idx = _draw(6, [300, 40], [300, 500], 4, 2, 128, 1000)
+    dq, dkc, dvc = _dev(q, kc, vc)
+    o, lse = attn.forward_paged(dq, dkc, dvc, _i32(qo), _i32(kv), _i32(idx), 300, True,
+                                128 ** -0.5, max_kvlen=2000, qo_indptr_host=qo,
+                                kv_indptr_host=kv, kv_indices_host=idx)
+    torch.cuda.synchronize()
+    ro, rl = oracle.attention_forward_paged(q, kc, vc, qo, kv, idx, True, 128 ** -0.5)
+    _check(o, lse, ro, rl, "prefill max_kvlen 2000")
 
 
 @pytest.mark.parametrize("name", list(wl.PAGED_WORKLOADS))
@@ -154,5 +182,6 @@ def test_full_paged_workload(name):
     if w.decode:
         _decode(x.q, x.k_cache, x.v_cache, x.kv_indptr, x.kv_indices, x.max_kvlen, w.scale, name)
     else:
-        _prefill(x.q, x.k_cache, x.v_cache, x.qo_indptr, x.kv_indptr, x.kv_indices, w.causal,
-                 w.scale, name)
+        for split in (True, False):
+            _prefill(x.q, x.k_cache, x.v_cache, x.qo_indptr, x.kv_indptr, x.kv_indices, w.causal,
+                     w.scale, f"{name} split={split}", split)

@@ -33,7 +33,9 @@ launches of the second pass (all on the stream the library launches on).
 Per-launch algorithmic FLOP of each kernel:
   fwd_kernel       2 GEMMs  (S = QK^T, O = PV)            = F
   bwd_dq_kernel    3 GEMMs  (S, dP = dO V^T, dQ = dS K)   = 1.5 F
-  bwd_dkdv_kernel  4 GEMMs  (S, dP, dV = P^T dO, dK)      = 2 F
+  dK/dV kernel     4 GEMMs  (S, dP, dV = P^T dO, dK)      = 2 F
+                   (bwd_dkdv4_kernel or bwd_dkdv_kernel, the form the library
+                   picks for the workload, attn_bwd_dkdv_form)
 with F the forward FLOP above.  `traffic` (HBM bytes per launch from
 rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a copy-kernel calibration) is
 read from profiles/traffic.json when that file was taken on the current
@@ -59,11 +61,11 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2516.6
 PEAK_HBM_GBS = 8000.0
 METRIC = "attention fwd/bwd TFLOP/s + % bf16 MFMA peak, B4 H16 S2048 D128 causal"
-KERNELS = ("fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel")
-GEMMS = {"fwd_kernel": 2, "bwd_dq_kernel": 3, "bwd_dkdv_kernel": 4}
+GEMMS = {"fwd_kernel": 2, "bwd_dq_kernel": 3, "bwd_dkdv_kernel": 4, "bwd_dkdv4_kernel": 4}
 KERNEL_SOURCES = {"fwd_kernel": "attn_fwd.hip", "fwd_kernel+fwd_merge_kernel": "attn_fwd.hip",
                   "bwd_dq_kernel": "attn_bwd.hip",
-                  "bwd_dkdv_kernel": "attn_bwd.hip", "decode_split_kernel": "attn_decode.hip",
+                  "bwd_dkdv_kernel": "attn_bwd.hip", "bwd_dkdv4_kernel": "attn_bwd.hip",
+                  "decode_split_kernel": "attn_decode.hip",
                   "decode_merge_kernel": "attn_decode.hip", "gemm_nt_kernel": "gemm.hip"}
 
 
@@ -473,8 +475,14 @@ def main(argv=None) -> int:
             if ev is not None:
                 ev[2 + i].record()
 
-    ms_step, kl = time_steps(step, len(KERNELS), args.steps, args.warmup)
-    kern_ms = dict(zip(KERNELS, kl))
+    # The dK/dV phase runs the form the library picks for these shapes.
+    nseg = len(x.cu_seqlens) - 1 if w.varlen else w.B
+    form = attn.attn_bwd_dkdv_form(nseg, w.Hkv, ms_len if w.varlen else w.S,
+                                   q.shape[0] if w.varlen else 0, w.D, w.causal, w.varlen)
+    dkdv = "bwd_dkdv4_kernel" if form == attn.ATTN_BWD_DKDV_TWO_PER_CU else "bwd_dkdv_kernel"
+    kernels = ("fwd_kernel", "bwd_dq_kernel", dkdv)
+    ms_step, kl = time_steps(step, len(kernels), args.steps, args.warmup)
+    kern_ms = dict(zip(kernels, kl))
     for t in (o, lse, dq, dk, dv):
         if not torch.isfinite(t.float()).all():
             print("non-finite output", file=sys.stderr)
@@ -483,10 +491,10 @@ def main(argv=None) -> int:
     F = fwd_flops(w, x.cu_seqlens)
     total = 3.5 * F
     value = total / (ms_step * 1e-3) / 1e12
-    dom = max(KERNELS, key=lambda n: kern_ms[n])
+    dom = max(kernels, key=lambda n: kern_ms[n])
     achieved = GEMMS[dom] / 2 * F / (kern_ms[dom] * 1e-3) / 1e12
     fwd_ms = kern_ms["fwd_kernel"]
-    bwd_ms = kern_ms["bwd_dq_kernel"] + kern_ms["bwd_dkdv_kernel"]
+    bwd_ms = kern_ms["bwd_dq_kernel"] + kern_ms[dkdv]
     cfg = {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "S": w.S, "D": w.D,
            "causal": w.causal, "seed": 0}
     if w.varlen:

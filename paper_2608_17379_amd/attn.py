@@ -25,12 +25,15 @@ STATUS_NAMES = {
 }
 EXPORTS = ("attn_fwd", "attn_bwd", "attn_bwd_workspace_size", "attn_fwd_varlen",
            "attn_bwd_varlen", "attn_bwd_varlen_workspace_size", "attn_bwd_phases",
-           "attn_bwd_varlen_phases", "attn_fwd_paged_workspace_size", "attn_fwd_paged",
+           "attn_bwd_varlen_phases", "attn_bwd_dkdv_form", "attn_fwd_paged_workspace_size",
+           "attn_fwd_paged",
            "attn_decode_paged_workspace_size",
            "attn_decode_paged", "attn_decode_paged_phases", "attn_gemm_bf16_nt",
            "attn_status_string")
 ATTN_BWD_DQ = 1
 ATTN_BWD_DKDV = 2
+ATTN_BWD_DKDV_ONE_PER_CU = 4
+ATTN_BWD_DKDV_TWO_PER_CU = 8
 ATTN_DECODE_SPLIT = 1
 ATTN_DECODE_MERGE = 2
 
@@ -68,6 +71,8 @@ def lib() -> ctypes.CDLL:
         l.attn_bwd_phases.restype = _I
         l.attn_bwd_varlen_phases.argtypes = [_P] * 10 + [_I] * 7 + [_F, _P, _Z, _I, _P]
         l.attn_bwd_varlen_phases.restype = _I
+        l.attn_bwd_dkdv_form.argtypes = [_I] * 7
+        l.attn_bwd_dkdv_form.restype = _I
         l.attn_fwd_paged_workspace_size.argtypes = [_I] * 7
         l.attn_fwd_paged_workspace_size.restype = _Z
         l.attn_fwd_paged.argtypes = [_P] * 8 + [_I] * 10 + [_F, _P, _Z, _P]
@@ -172,6 +177,16 @@ def attn_bwd(q, k, v, o, lse, dO, dq, dk, dv, causal: bool, scale: float,
                         float(scale), _ptr(workspace, "workspace", torch.uint8),
                         workspace.numel(), _stream(stream))
     _check(st, "attn_bwd")
+
+
+def attn_bwd_dkdv_form(nseg: int, Hkv: int, S: int, total: int, D: int, causal: bool,
+                       packed: bool) -> int:
+    """The dK/dV form the library picks (ATTN_BWD_DKDV_ONE_PER_CU or
+    ATTN_BWD_DKDV_TWO_PER_CU; 0 at D = 64)."""
+    st = lib().attn_bwd_dkdv_form(nseg, Hkv, S, total, D, int(bool(causal)), int(bool(packed)))
+    if st < 0:
+        _check(st, "attn_bwd_dkdv_form")
+    return st
 
 
 # --------------------------------------------------------------------------
@@ -443,12 +458,21 @@ def workspace_for(q, k, cu_seqlens=None) -> torch.Tensor:
 
 
 def backward(q, k, v, o, lse, dO, causal: bool, scale: float, cu_seqlens=None,
-             max_seqlen: int = 0, workspace=None, cu_seqlens_host=None):
-    """Return (dq, dk, dv) for fixed-length or packed inputs."""
+             max_seqlen: int = 0, workspace=None, cu_seqlens_host=None, dkdv_form: int = 0):
+    """Return (dq, dk, dv) for fixed-length or packed inputs.  dkdv_form 0
+    lets the library choose the dK/dV kernel's form; ATTN_BWD_DKDV_ONE_PER_CU
+    or ATTN_BWD_DKDV_TWO_PER_CU forces one."""
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     ws = workspace if workspace is not None else workspace_for(q, k, cu_seqlens)
+    phases = ATTN_BWD_DQ | ATTN_BWD_DKDV | int(dkdv_form)
     if cu_seqlens is None:
-        attn_bwd(q, k, v, o, lse, dO, dq, dk, dv, causal, scale, ws)
+        if dkdv_form:
+            attn_bwd_phases(q, k, v, o, lse, dO, dq, dk, dv, causal, scale, ws, phases)
+        else:
+            attn_bwd(q, k, v, o, lse, dO, dq, dk, dv, causal, scale, ws)
+    elif dkdv_form:
+        attn_bwd_varlen_phases(q, k, v, o, lse, dO, dq, dk, dv, cu_seqlens, max_seqlen, causal,
+                               scale, ws, phases, cu_seqlens_host=cu_seqlens_host)
     else:
         attn_bwd_varlen(q, k, v, o, lse, dO, dq, dk, dv, cu_seqlens, max_seqlen, causal, scale,
                         ws, cu_seqlens_host=cu_seqlens_host)

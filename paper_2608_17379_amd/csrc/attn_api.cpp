@@ -121,11 +121,20 @@ int fwd_common(const void* q, const void* k, const void* v, void* o, float* lse,
   return attn::launch_fwd(a, D, stream) == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
 }
 
+// A backward phase mask: at least one kernel, and at most one dK/dV form
+// bit, given only with the dK/dV phase.
+bool valid_bwd_phases(int phases) {
+  if (phases < 1 || phases > 15 || (phases & 3) == 0) return false;
+  const int form = phases & (ATTN_BWD_DKDV_ONE_PER_CU | ATTN_BWD_DKDV_TWO_PER_CU);
+  if (form == (ATTN_BWD_DKDV_ONE_PER_CU | ATTN_BWD_DKDV_TWO_PER_CU)) return false;
+  return form == 0 || (phases & ATTN_BWD_DKDV) != 0;
+}
+
 int bwd_common(const void* q, const void* k, const void* v, const void* o, const float* lse,
                const void* dO, void* dq, void* dk, void* dv, const Layout& L, int D, int causal,
                float scale, void* ws, size_t ws_bytes, size_t ws_need, int phases,
                hipStream_t stream) {
-  if (phases < 1 || phases > 3) return ATTN_ERR_VALUE;
+  if (!valid_bwd_phases(phases)) return ATTN_ERR_VALUE;
   if (any_null({q, k, v, o, lse, dO, dq, dk, dv})) return ATTN_ERR_NULL;
   if (any_misaligned({q, k, v, o, lse, dO, dq, dk, dv})) return ATTN_ERR_ALIGN;
   if (!ws || ws_bytes < ws_need) return ATTN_ERR_WORKSPACE;
@@ -146,7 +155,8 @@ int bwd_common(const void* q, const void* k, const void* v, const void* o, const
   a.scale = scale;
   a.scale_log2 = scale * 1.4426950408889634f;
   a.causal = causal;
-  return attn::launch_bwd(a, D, phases, stream) == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
+  a.dkdv_form = (phases & ATTN_BWD_DKDV_ONE_PER_CU) ? 1 : (phases & ATTN_BWD_DKDV_TWO_PER_CU) ? 2 : 0;
+  return attn::launch_bwd(a, D, phases & 3, stream) == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
 }
 
 // A paged cache must be addressable with 31-bit byte offsets from the start
@@ -170,7 +180,7 @@ size_t round256(int64_t bytes) { return (size_t)((bytes + 255) / 256 * 256); }
 // MI355X has CUs is split into chunks of keys, when its requests are longer
 // than one chunk.  The rule uses the part's CU count, not a device query, so
 // that the workspace size depends on the shapes alone.
-constexpr int kChipCUs = 256;
+using attn::kChipCUs;
 
 int paged_split(int batch, int max_qlen, int max_kvlen, int Hq) {
   const int64_t nqt = ((int64_t)max_qlen + attn::kFwdBlockRows - 1) / attn::kFwdBlockRows;
@@ -206,6 +216,17 @@ size_t attn_bwd_workspace_size(int B, int Hq, int Hkv, int S, int D) {
   return delta_bytes((int64_t)B * Hq * S);
 }
 
+int attn_bwd_dkdv_form(int nseg, int Hkv, int S, int total, int D, int causal, int packed) {
+  if (nseg < 0 || Hkv < 1 || S < 0 || total < 0) return ATTN_ERR_SHAPE;
+  if (D != 64 && D != 96 && D != 128) return ATTN_ERR_HEAD_DIM;
+  if ((causal != 0 && causal != 1) || (packed != 0 && packed != 1)) return ATTN_ERR_VALUE;
+  switch (attn::dkdv_form_for(nseg, Hkv, S, total, packed != 0, D, causal != 0)) {
+    case 1: return ATTN_BWD_DKDV_ONE_PER_CU;
+    case 2: return ATTN_BWD_DKDV_TWO_PER_CU;
+    default: return 0;
+  }
+}
+
 int attn_bwd_phases(const void* q, const void* k, const void* v, const void* o, const float* lse,
                     const void* dO, void* dq, void* dk, void* dv, int B, int Hq, int Hkv, int S,
                     int D, int causal, float scale, void* workspace, size_t workspace_bytes,
@@ -214,7 +235,7 @@ int attn_bwd_phases(const void* q, const void* k, const void* v, const void* o, 
   if (st != ATTN_OK) return st;
   if (B < 0 || check_rows(S) != ATTN_OK) return ATTN_ERR_SHAPE;
   if ((int64_t)B * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
-  if (phases < 1 || phases > 3) return ATTN_ERR_VALUE;
+  if (!valid_bwd_phases(phases)) return ATTN_ERR_VALUE;
   if (B == 0 || S == 0) return ATTN_OK;
   return bwd_common(q, k, v, o, lse, dO, dq, dk, dv, fixed_layout(B, Hq, Hkv, S, D), D, causal,
                     scale, workspace, workspace_bytes, attn_bwd_workspace_size(B, Hq, Hkv, S, D),
@@ -260,7 +281,7 @@ int attn_bwd_varlen_phases(const void* q, const void* k, const void* v, const vo
   if (st != ATTN_OK) return st;
   if (nseq < 0 || total < 0 || check_rows(max_seqlen) != ATTN_OK) return ATTN_ERR_SHAPE;
   if ((int64_t)nseq * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
-  if (phases < 1 || phases > 3) return ATTN_ERR_VALUE;
+  if (!valid_bwd_phases(phases)) return ATTN_ERR_VALUE;
   if (nseq == 0 || total == 0) return ATTN_OK;
   if (max_seqlen < 1) return ATTN_ERR_VALUE;
   if (!cu_seqlens) return ATTN_ERR_NULL;

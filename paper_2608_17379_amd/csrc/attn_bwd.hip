@@ -14,13 +14,17 @@
 //    dO and O are read once) and stores it, with L log2(e), in the
 //    workspace; the loop over key tiles recomputes S^T = K Q^T and
 //    dP^T = V dO^T, forms dS^T in registers and accumulates dQ^T += K^T dS^T.
-//  * bwd_dkdv_kernel: one workgroup per (segment, key/value head, 128 keys)
-//    (8 wavefronts at D = 128 and 96, 4 at D = 64), launched after bwd_dq_kernel
-//    (it reads the workspace).  The workgroup keeps its K and V rows in LDS
-//    and loops over every query head of the group and every query tile that
-//    can see its keys, accumulating dV^T += dO^T P and dK^T += Q^T dS in
-//    registers; the grouped-query sum therefore needs no cross-workgroup
-//    reduction.
+//  * bwd_dkdv_kernel / bwd_dkdv4_kernel: one workgroup per (segment,
+//    key/value head, 128 keys), launched after bwd_dq_kernel (they read the
+//    workspace).  The workgroup keeps its keys' K and V rows on chip (LDS,
+//    or K in registers) and loops over every query head of the group and
+//    every query tile that can see its keys, accumulating dV^T += dO^T P and
+//    dK^T += Q^T dS in registers; the grouped-query sum therefore needs no
+//    cross-workgroup reduction.  At D = 128 and 96 there are two forms:
+//    bwd_dkdv_kernel with 8 wavefronts and one workgroup per CU, and
+//    bwd_dkdv4_kernel with 4 wavefronts and two per CU (chosen by the grid,
+//    see launch_bwd_d); at D = 64 bwd_dkdv_kernel has 4 wavefronts and two
+//    workgroups per CU.
 //
 // Tiles of 64 rows (K and V for dQ; Q, dO, L log2 e and Delta for dK/dV) go
 // from global memory straight into a ring of LDS stages (buffer_load ... lds,
@@ -561,6 +565,235 @@ __global__ __launch_bounds__(64 * dkv_waves<D>(), D == 64 ? 2 : 1) void bwd_dkdv
   }
 }
 
+// ---------------------------------------------------------------------------
+// dK, dV at D = 128 and D = 96: four wavefronts per 128 keys, two workgroups
+// per CU.  Each wavefront owns 32 keys outright (no partial to combine): its
+// K rows stay in registers as the B operand of S = Q K^T, the workgroup's V
+// rows in LDS (B operand of dP = dO V^T), and the query side streams through
+// two LDS stages of 32 rows.  64.5 KiB of LDS per workgroup, so the two
+// wavefronts on a SIMD come from different workgroups.
+// ---------------------------------------------------------------------------
+constexpr int kQS = 32;   // query rows per step
+
+template <int D>
+struct Dkv4Smem {
+  static constexpr int P = lds_pitch<D>();
+  static constexpr int TILE = 64 * P * 2;   // bytes of a 64-row bf16 tile
+  static constexpr int HT = kQS * P * 2;    // bytes of a 32-row bf16 tile
+  static constexpr int V = 0;               // 2 tiles: keys 0-63, 64-127
+  static constexpr int Q = V + 2 * TILE;    // 2 stages
+  static constexpr int DO = Q + 2 * HT;     // 2 stages
+  static constexpr int LSE = DO + 2 * HT;   // 2 stages x 32 fp32
+  static constexpr int DEL = LSE + 2 * kQS * 4;
+  static constexpr int BYTES = DEL + 2 * kQS * 4;
+  static_assert(4 * 2 * 32 * P * 2 <= BYTES, "epilogue staging");
+};
+
+template <int D, bool CAUSAL>
+__global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
+  using SM = Dkv4Smem<D>;
+  constexpr int P = SM::P;
+  using VTile = AsyncTile<D, 4>;   // a 64-row tile, four wavefronts
+  using HTile = AsyncTile<D, 8>;   // wavefronts 0-3 of eight: rows 0-31 of a tile
+  __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
+  const uint16_t* const sv = reinterpret_cast<const uint16_t*>(smem + SM::V);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = wave_id();
+  const int l32 = lane & 31, half = lane >> 5;
+  const int kq = wave;   // 32-key group
+
+  const Layout L = a.L;
+  const int z = blockIdx.x / L.Hkv, hk = blockIdx.x % L.Hkv;
+  const Segment seg = segment_of(L, z);
+  const int k0 = (int)blockIdx.y * kKN;   // lowest keys (most work) first
+  if (k0 >= seg.len) return;
+
+  const int64_t kvoff = (int64_t)seg.start * L.kv_row + (int64_t)z * L.kv_batch +
+                        (int64_t)hk * L.kv_head;
+  const int64_t qseg = (int64_t)seg.start * L.q_row + (int64_t)z * L.q_batch;
+  const int64_t rseg = (int64_t)seg.start + (int64_t)z * L.r_batch;
+  const int kw0 = k0 + 32 * kq;
+  const int krow = kw0 + l32;
+  const uint16_t* const qbase = a.q;
+  const uint16_t* const dobase = a.dout;
+  const float* const lsebase = a.lse2;
+  const float* const delbase = a.delta;
+  const int group = L.group;
+  const int64_t q_head = L.q_head, r_head = L.r_head;
+  const int64_t q_row_b = L.q_row * 2;
+  const int len = seg.len;
+  const float sl2 = a.scale_log2;
+
+  // Steps run over (group head g, 32-query step j), from the step holding
+  // key k0 (causal) to the segment end.
+  const int it0 = CAUSAL ? k0 / kQS : 0;
+  const int nqs = (seg.len + kQS - 1) / kQS;
+  const int per_head = nqs - it0;
+  const int niter = per_head * L.group;
+
+  const HTile qdma(wave, lane, (int)q_row_b);
+  const RowReader<D> rr(l32, half);
+  const TransReader<D> trr(lane);
+  const uint32_t sbase = lds_addr(smem);
+
+  // V rows of the workgroup into LDS (once); this wavefront's K rows into
+  // registers: kreg[c] = K[krow][16 c + 8 half .. + 7] (zero past the end).
+  {
+    const VTile vdma(wave, lane, (int)(L.kv_row * 2));
+    const int64_t kv_row_b = L.kv_row * 2;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+      dma_tile<D>(vdma, rows_desc(a.v + kvoff, k0 + 64 * t, len, kv_row_b),
+                  sbase + SM::V + t * SM::TILE, wave);
+  }
+  u32x4 kreg[D / 16];
+  {
+    const rsrc_t rk = rows_rsrc(a.k + kvoff, kw0, len, L.kv_row);
+    const int base = l32 * (int)(L.kv_row * 2) + 16 * half;
+#pragma unroll
+    for (int c = 0; c < D / 16; ++c) kreg[c] = bload16(rk, base + 32 * c);
+  }
+
+  auto issue = [&](int n, int st) __attribute__((always_inline)) {
+    const int g = n / per_head;
+    const int qb = (it0 + n % per_head) * kQS;
+    const int h = hk * group + g;
+    const int64_t qoff = qseg + (int64_t)h * q_head;
+    dma_tile<D>(qdma, rows_desc(qbase + qoff, qb, len, q_row_b), sbase + SM::Q + st * SM::HT,
+                wave);
+    dma_tile<D>(qdma, rows_desc(dobase + qoff, qb, len, q_row_b), sbase + SM::DO + st * SM::HT,
+                wave);
+    if (wave == 0 && lane < 8) {
+      const int64_t r = rseg + (int64_t)h * r_head;
+      dma16(rows_desc(lsebase + r, qb, len, 4), sbase + SM::LSE + st * (kQS * 4), 16 * lane);
+      dma16(rows_desc(delbase + r, qb, len, 4), sbase + SM::DEL + st * (kQS * 4), 16 * lane);
+    }
+  };
+
+  f32x16 dkacc[D / 32], dvacc[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      dkacc[db][r] = 0.f;
+      dvacc[db][r] = 0.f;
+    }
+  // This wavefront's V rows: tile kq / 2, rows 32 (kq % 2) + l32.
+  const uint16_t* const vrd = sv + (kq >> 1) * (SM::TILE / 2) + 32 * (kq & 1) * P;
+
+  // The 32 queries of step n (stage st) against this wavefront's 32 keys.
+  auto compute = [&](int n, int st, auto masked) __attribute__((always_inline)) {
+    const uint16_t* q = reinterpret_cast<const uint16_t*>(smem + SM::Q + st * SM::HT);
+    const uint16_t* dout = reinterpret_cast<const uint16_t*>(smem + SM::DO + st * SM::HT);
+    const float* lse = reinterpret_cast<const float*>(smem + SM::LSE + st * (kQS * 4));
+    const float* del = reinterpret_cast<const float*>(smem + SM::DEL + st * (kQS * 4));
+    const int qs0 = (it0 + n % per_head) * kQS;
+    f32x16 s, dp;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      s[r] = 0.f;
+      dp[r] = 0.f;
+    }
+#pragma unroll
+    for (int c = 0; c < D / 16; ++c) {
+      s = mfma32(ld16(q + rr.rm[c]), kreg[c], s);
+      dp = mfma32(ld16(dout + rr.rm[c]), ld16(vrd + rr.rm[c]), dp);
+      // Keep at most four chunks of operands in flight (register budget).
+      if (c % 4 == 3) __builtin_amdgcn_sched_barrier(0);
+    }
+    // s[r], dp[r]: query qs0 + 8(r/4) + 4half + r%4, key krow.
+    const int t = krow - qs0 - 4 * half;   // key minus the lane's first query
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse[8 * g + 4 * half]);
+      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&del[8 * g + 4 * half]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 4 * g + i;
+        float p = fast_exp2(__builtin_fmaf(s[r], sl2, -l4[i]));
+        if constexpr (decltype(masked)::value) p = t > 8 * g + i ? 0.f : p;   // key after query
+        s[r] = p;
+        dp[r] = p * (dp[r] - d4[i]);
+      }
+    }
+    // dV^T += dO^T P, dK^T += Q^T dS (A operands read transposed).
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const u32x4 pb = pack_chunk(s, c);
+      const u32x4 dsb = pack_chunk(dp, c);
+      const int rc = 16 * c * P;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        const u32x2 dlo = ld_tr(dout + trr.tr[db][0] + rc), dhi = ld_tr(dout + trr.tr[db][1] + rc);
+        dvacc[db] = mfma32(u32x4{dlo[0], dlo[1], dhi[0], dhi[1]}, pb, dvacc[db]);
+        const u32x2 qlo = ld_tr(q + trr.tr[db][0] + rc), qhi = ld_tr(q + trr.tr[db][1] + rc);
+        dkacc[db] = mfma32(u32x4{qlo[0], qlo[1], qhi[0], qhi[1]}, dsb, dkacc[db]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // Step n: its copies have landed for this wavefront; the barrier makes
+  // every wavefront's share visible and frees the stage read at n - 1, which
+  // the copies of step n + 1 now fill.  Under the causal mask a wavefront
+  // skips the steps whose queries all precede its keys and masks the one
+  // holding its diagonal.
+  auto sync = [&](int n) __attribute__((always_inline)) {
+    wait_vm_all();
+    __syncthreads();
+    if (n + 1 < niter) issue(n + 1, (n + 1) & 1);
+  };
+  // Per head: under the causal mask the first four steps hold the
+  // workgroup's diagonal (masked compute, skipped by the wavefronts whose
+  // keys all follow the step's queries); the rest need no mask.  Each loop
+  // body has one form of compute (two forms in one body exceed the register
+  // budget).
+  const int ndiag = CAUSAL ? min(kKN / kQS, per_head) : 0;
+  issue(0, 0);
+  int n = 0;
+#pragma nounroll
+  for (int g = 0; g < group; ++g) {
+#pragma nounroll
+    for (const int nd = n + ndiag; n < nd; ++n) {
+      sync(n);
+      if ((it0 + n % per_head) * kQS >= kw0) compute(n, n & 1, std::true_type{});
+    }
+#pragma nounroll
+    for (const int ne = (g + 1) * per_head; n < ne; ++n) {
+      sync(n);
+      compute(n, n & 1, std::false_type{});
+    }
+  }
+
+  // Epilogue: each wavefront stages its bf16 dK and dV rows in LDS ([32
+  // keys][D], 16-byte chunks swizzled by row) and writes whole rows.
+  __syncthreads();   // every wavefront is done with the stages
+  const int64_t kv_row = L.kv_row;
+  auto store_rows = [&](const f32x16 (&acc)[D / 32], float mul, uint16_t* stg, uint16_t* gout)
+      __attribute__((always_inline)) {
+    const int sw = tile_swz<P>(l32);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        st8(stg + l32 * P + 8 * ((4 * db + g) ^ sw) + 4 * half,
+            u32x2{pack_bf16(acc[db][4 * g] * mul, acc[db][4 * g + 1] * mul),
+                  pack_bf16(acc[db][4 * g + 2] * mul, acc[db][4 * g + 3] * mul)});
+    constexpr int CPR = D / 8;
+#pragma unroll
+    for (int i = 0; i < 32 * CPR / 64; ++i) {
+      const int pidx = i * 64 + lane;
+      const int row = pidx / CPR, ch = pidx % CPR;
+      const u32x4 v = ld16(stg + row * P + 8 * (ch ^ tile_swz<P>(row)));
+      if (kw0 + row < len) st16(gout + (int64_t)(kw0 + row) * kv_row + 8 * ch, v);
+    }
+  };
+  uint16_t* stg = reinterpret_cast<uint16_t*>(smem) + wave * 2 * 32 * P;
+  store_rows(dkacc, a.scale, stg, a.dk + kvoff);
+  store_rows(dvacc, 1.f, stg + 32 * P, a.dv + kvoff);
+}
+
 // Explicit instantiations: without them the host compiler may skip the
 // launch stubs of these templates (leaving undefined symbols in the library).
 template __global__ void bwd_dq_kernel<64, false>(BwdArgs);
@@ -575,6 +808,10 @@ template __global__ void bwd_dkdv_kernel<96, false>(BwdArgs);
 template __global__ void bwd_dkdv_kernel<96, true>(BwdArgs);
 template __global__ void bwd_dkdv_kernel<128, false>(BwdArgs);
 template __global__ void bwd_dkdv_kernel<128, true>(BwdArgs);
+template __global__ void bwd_dkdv4_kernel<96, false>(BwdArgs);
+template __global__ void bwd_dkdv4_kernel<96, true>(BwdArgs);
+template __global__ void bwd_dkdv4_kernel<128, false>(BwdArgs);
+template __global__ void bwd_dkdv4_kernel<128, true>(BwdArgs);
 
 }  // namespace
 
@@ -592,6 +829,18 @@ void launch_bwd_d(const BwdArgs& a, int phases, hipStream_t stream) {
       hipLaunchKernelGGL((bwd_dq_kernel<D, false>), gq, dim3(kDqThreads), 0, stream, a);
   }
   if (phases & 2) {
+    if constexpr (D != 64) {
+      const int form = a.dkdv_form ? a.dkdv_form
+                                   : dkdv_form_for(a.L.nseg, a.L.Hkv, a.L.S, a.L.total,
+                                                   a.L.cu != nullptr, D, a.causal != 0);
+      if (form == 2) {
+        if (a.causal)
+          hipLaunchKernelGGL((bwd_dkdv4_kernel<D, true>), gk, dim3(256), 0, stream, a);
+        else
+          hipLaunchKernelGGL((bwd_dkdv4_kernel<D, false>), gk, dim3(256), 0, stream, a);
+        return;
+      }
+    }
     if (a.causal)
       hipLaunchKernelGGL((bwd_dkdv_kernel<D, true>), gk, dim3(64 * dkv_waves<D>()), 0, stream, a);
     else
@@ -600,6 +849,18 @@ void launch_bwd_d(const BwdArgs& a, int phases, hipStream_t stream) {
 }
 
 }  // namespace
+
+// Two workgroups per CU keep every workgroup of a grid resident from the
+// start, so the unequal work of causal key blocks is only balanced (heaviest
+// first) when there are at least two rounds of them; fewer go to the
+// one-per-CU form.  Packed layouts count their sequences' blocks, about
+// total / 128 + nseq per key head.
+int dkdv_form_for(int nseg, int Hkv, int S, int total, bool packed, int D, bool causal) {
+  if (D == 64) return 0;
+  const int64_t blocks = packed ? (int64_t)Hkv * (total / kKN + nseg)
+                                : (int64_t)nseg * Hkv * ((S + kKN - 1) / kKN);
+  return !causal || blocks >= 4 * kChipCUs ? 2 : 1;
+}
 
 hipError_t launch_bwd(const BwdArgs& a, int D, int phases, hipStream_t stream) {
   if (D == 64)

@@ -73,6 +73,7 @@ struct BwdArgs {
   float scale;             // softmax scale
   float scale_log2;        // scale * log2(e)
   int causal;
+  int dkdv_form;           // D = 96, 128: 0 chosen by the grid, 1 one, 2 two workgroups per CU
 };
 
 // Paged decode: one query row per request (q, o [batch, Hq, D], lse
@@ -110,11 +111,15 @@ hipError_t launch_gemm(const GemmArgs& g, int cus, hipStream_t stream);
 hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream);
 // Keys per chunk of the decode split (sizes the workspace).
 constexpr int kDecodeChunk = 64;
+constexpr int kChipCUs = 256;        // compute units of the MI355X
 constexpr int kFwdSplitKeys = 256;   // keys per chunk of a split paged prefill
 constexpr int kFwdBlockRows = 128;   // query rows per forward workgroup
 // phases: bit 0 = split kernel, bit 1 = merge kernel.
 hipError_t launch_decode(const DecodeArgs& a, int D, int phases, hipStream_t stream);
 // phases: bit 0 = Delta and dQ kernel, bit 1 = dK/dV kernel.
 hipError_t launch_bwd(const BwdArgs& a, int D, int phases, hipStream_t stream);
+// The dK/dV form launch_bwd picks when BwdArgs::dkdv_form is 0: 1 (one
+// workgroup per CU) or 2 (two per CU) at D = 96 and 128, 0 at D = 64.
+int dkdv_form_for(int nseg, int Hkv, int S, int total, bool packed, int D, bool causal);
 
 }  // namespace attn

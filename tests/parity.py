@@ -50,13 +50,13 @@ def to_gpu(x: wl.Inputs):
     return q, k, v, do, cu
 
 
-def gpu_fwd_bwd(x: wl.Inputs, causal: bool, scale: float):
+def gpu_fwd_bwd(x: wl.Inputs, causal: bool, scale: float, dkdv_form: int = 0):
     q, k, v, do, cu = to_gpu(x)
     ms = x.max_seqlen if cu is not None else 0
     o, lse = attn.forward(q, k, v, causal, scale, cu_seqlens=cu, max_seqlen=ms,
                           cu_seqlens_host=x.cu_seqlens)
     dq, dk, dv = attn.backward(q, k, v, o, lse, do, causal, scale, cu_seqlens=cu, max_seqlen=ms,
-                               cu_seqlens_host=x.cu_seqlens)
+                               cu_seqlens_host=x.cu_seqlens, dkdv_form=dkdv_form)
     torch.cuda.synchronize()
     return o.cpu(), lse.cpu(), dq.cpu(), dk.cpu(), dv.cpu()
 

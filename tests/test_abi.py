@@ -22,10 +22,12 @@ def header_symbols():
 def test_phase_mask_validation():
     l = attn.lib()
     args = [A] * 9 + [1, 2, 2, 64, 64, 1, 0.125, A, 1 << 20]
-    for bad in (0, 4, -1):
+    # 4 and 8 pick the dK/dV form: only with the dK/dV phase, never both
+    bad_masks = (0, 4, 8, 12, -1, 16, 5, 9, 13, 14, 15)
+    for bad in bad_masks:
         assert l.attn_bwd_phases(*args, bad, None) == -8
     argsv = [A] * 10 + [2, 64, 100, 2, 1, 128, 1, 0.1, A, 1 << 20]
-    for bad in (0, 4):
+    for bad in bad_masks:
         assert l.attn_bwd_varlen_phases(*argsv, bad, None) == -8
     assert l.attn_bwd_phases(*(args[:-2] + [A, 1]), 2, None) == -6
 
@@ -253,3 +255,20 @@ def test_gemm_validation():
 def test_gemm_empty_k_allows_null_operands():
     l = attn.lib()
     assert l.attn_gemm_bf16_nt(A, A, 0, 64, 64, 0, None) == -1   # c is still needed
+
+
+def test_dkdv_form_rule():
+    form = attn.attn_bwd_dkdv_form
+    one, two = attn.ATTN_BWD_DKDV_ONE_PER_CU, attn.ATTN_BWD_DKDV_TWO_PER_CU
+    assert form(4, 16, 2048, 0, 128, True, False) == two      # 1024 causal key blocks
+    assert form(2, 8, 4096, 0, 128, True, False) == one       # 512: one round at two per CU
+    assert form(2, 8, 4096, 0, 128, False, False) == two      # non-causal blocks are equal
+    assert form(1, 16, 16384, 0, 96, True, False) == two
+    assert form(33, 4, 1500, 16294, 128, True, True) == one   # ~640 packed blocks
+    assert form(4, 48, 4096, 0, 64, True, False) == 0         # D = 64: one form
+    l = attn.lib()
+    assert l.attn_bwd_dkdv_form(1, 1, 128, 0, 80, 1, 0) == -4
+    assert l.attn_bwd_dkdv_form(-1, 1, 128, 0, 128, 1, 0) == -2
+    assert l.attn_bwd_dkdv_form(1, 1, 128, 0, 128, 2, 0) == -8
+    with pytest.raises(attn.AttnError):
+        form(1, 1, 128, 0, 80, True, False)

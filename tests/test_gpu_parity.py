@@ -23,12 +23,12 @@ from parity import (GRAD_RELL2, LSE_MAXABS, O_MAXABS, announce, check_all, gpu_f
 pytestmark = pytest.mark.gpu
 
 
-def _fixed_case(S, D, causal, Hq=2, Hkv=2, B=1, seed=0, qk_mult=1.0):
+def _fixed_case(S, D, causal, Hq=2, Hkv=2, B=1, seed=0, qk_mult=1.0, dkdv_form=0):
     w = wl.small(f"b{B}_hq{Hq}_hkv{Hkv}_s{S}_d{D}_c{int(causal)}", B, Hq, Hkv, S, D, causal,
                  qk_mult=qk_mult)
     x = wl.make_inputs(w, seed)
-    announce(f"fixed {w.name} seed={seed}")
-    got = gpu_fwd_bwd(x, causal, w.scale)
+    announce(f"fixed {w.name} seed={seed} dkdv_form={dkdv_form}")
+    got = gpu_fwd_bwd(x, causal, w.scale, dkdv_form)
     ref = oracle_all(x, causal, w.scale)
     return check_all(got, ref, w.name)
 
@@ -61,6 +61,29 @@ def test_long_ragged_sequence(D):
 
 def test_peaky_rows():
     _fixed_case(300, 128, True, qk_mult=4.0)
+
+
+FORMS = [attn.ATTN_BWD_DKDV_ONE_PER_CU, attn.ATTN_BWD_DKDV_TWO_PER_CU]
+
+
+@pytest.mark.parametrize("form", FORMS)
+@pytest.mark.parametrize("D", [96, 128])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("S", [17, 65, 129, 383])
+def test_dkdv_forms(S, causal, D, form):
+    """Both forms of the dK/dV kernel, whichever the library would pick:
+    tails inside the first and later key blocks and the causal diagonal."""
+    _fixed_case(S, D, causal, dkdv_form=form)
+
+
+@pytest.mark.parametrize("form", FORMS)
+@pytest.mark.parametrize("D", [96, 128])
+def test_dkdv_forms_gqa_and_packed(D, form):
+    _fixed_case(190, D, True, Hq=8, Hkv=2, B=2, dkdv_form=form)
+    w = wl.small(f"varlen_forms_d{D}", 6, 4, 1, 300, D, True, varlen=True)
+    x = wl.make_inputs(w, 3, lengths=[1, 17, 64, 0, 130, 300])
+    announce(f"packed {w.name} dkdv_form={form}")
+    check_all(gpu_fwd_bwd(x, True, w.scale, form), oracle_all(x, True, w.scale), w.name)
 
 
 @pytest.mark.parametrize("D", [64, 96, 128])

@@ -76,6 +76,29 @@ def test_dkdv_forms(S, causal, D, form):
     _fixed_case(S, D, causal, dkdv_form=form)
 
 
+def test_dkdv_phase_repeated_after_one_dq_phase():
+    """A second dK/dV phase on the workspace of one dQ phase gives the same
+    bits (the dK/dV kernels only read the workspace)."""
+    w = wl.small("dkdv_repeat", 2, 4, 2, 700, 128, True)
+    x = wl.make_inputs(w, 7)
+    q, k, v, do, _ = to_gpu(x)
+    o, lse = attn.forward(q, k, v, True, w.scale)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = attn.workspace_for(q, k)
+    two = attn.ATTN_BWD_DKDV | attn.ATTN_BWD_DKDV_TWO_PER_CU
+    attn.attn_bwd_phases(q, k, v, o, lse, do, dq, dk, dv, True, w.scale, ws, attn.ATTN_BWD_DQ)
+    attn.attn_bwd_phases(q, k, v, o, lse, do, dq, dk, dv, True, w.scale, ws, two)
+    torch.cuda.synchronize()
+    first = (dk.clone(), dv.clone())
+    dk.zero_()
+    dv.zero_()
+    attn.attn_bwd_phases(q, k, v, o, lse, do, dq, dk, dv, True, w.scale, ws, two)
+    torch.cuda.synchronize()
+    assert torch.equal(first[0], dk) and torch.equal(first[1], dv)
+    ref = oracle_all(x, True, w.scale)
+    check_all((o.cpu(), lse.cpu(), dq.cpu(), dk.cpu(), dv.cpu()), ref, "dkdv repeated")
+
+
 @pytest.mark.parametrize("form", FORMS)
 @pytest.mark.parametrize("D", [96, 128])
 def test_dkdv_forms_gqa_and_packed(D, form):

@@ -139,7 +139,7 @@ int bwd_common(const void* q, const void* k, const void* v, const void* o, const
   if (any_misaligned({q, k, v, o, lse, dO, dq, dk, dv})) return ATTN_ERR_ALIGN;
   if (!ws || ws_bytes < ws_need) return ATTN_ERR_WORKSPACE;
   if (misaligned(ws)) return ATTN_ERR_ALIGN;
-  attn::BwdArgs a;
+  attn::BwdArgs a{};
   a.L = L;
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);

@@ -22,6 +22,13 @@ timing is the GPU's, not the host's launch rate.  The K timed steps carry no
 events inside them; a second pass of K steps, not part of `value`, records
 an event around every launch for the per-kernel times.
 
+Two secondary objects: "cold" (fwd+bwd workloads) is the median of
+--cold-steps single steps, each started after a 512 MiB write has flushed the
+L2 caches and the MALL (the write is not timed); "gpu_state" is the graphics
+clock (mean over the XCDs), hotspot temperature and socket power sampled
+through amdsmi during an untimed pass of --state-seconds of back-to-back
+steps after the timed ones (null when amdsmi is not usable).
+
 FLOP convention: forward 4*B*Hq*S^2*D (halved when causal; packed input sums
 L^2 over sequences), backward 2.5x forward.  TFLOP/s = (forward + backward
 FLOP) / step time.  Peak: 2516.6 TFLOP/s dense bf16 MFMA (256 CUs x 2.4 GHz
@@ -161,6 +168,119 @@ def hold_gpu_for_enqueue(host_ms_per_step: float, steps: int) -> None:
     torch.cuda._sleep(int(cycles_per_ms * want_ms))
 
 
+class GpuMonitor:
+    """Samples the GPU's firmware metrics through amdsmi in a background
+    thread: graphics clock (MHz, mean over the XCDs), hotspot temperature (C)
+    and socket power (W).  The firmware refreshes them every few hundred
+    milliseconds, so they describe a sustained run, not a short one.
+    Monitoring never fails the benchmark: without amdsmi, or when a query
+    fails, the summary is None or lacks that field."""
+
+    def __init__(self, period_s: float = 0.01):
+        self.period = period_s
+        self.samples = []   # (gfx activity %, {quantity: value})
+        self._stop = None
+        self._thread = None
+        self._smi = None
+        self._h = None
+
+    def _sample(self):
+        try:
+            m = self._smi.amdsmi_get_gpu_metrics_info(self._h)
+        except Exception:
+            return
+        clks = m.get("current_gfxclks")
+        if isinstance(clks, list):
+            clks = [c for c in clks if isinstance(c, (int, float)) and 0 < c < 10000]
+        vals = {"sclk_mhz": sum(clks) / len(clks) if clks else m.get("current_gfxclk"),
+                "temp_c": m.get("temperature_hotspot"), "power_w": m.get("current_socket_power")}
+        act = m.get("average_gfx_activity")
+        self.samples.append((act if isinstance(act, (int, float)) else None,
+                             {k: float(v) for k, v in vals.items()
+                              if isinstance(v, (int, float)) and v == v}))
+
+    def __enter__(self):
+        import threading
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            self._smi = amdsmi
+            self._h = amdsmi.amdsmi_get_processor_handles()[0]
+        except Exception:
+            self._smi = None
+            return self
+        self._stop = threading.Event()
+
+        def loop():
+            while not self._stop.is_set():
+                self._sample()
+                self._stop.wait(self.period)
+        self._thread = threading.Thread(target=loop, daemon=True)
+        self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        if self._thread is not None:
+            self._stop.set()
+            self._thread.join()
+        if self._smi is not None:
+            try:
+                self._smi.amdsmi_shut_down()
+            except Exception:
+                pass
+        return False
+
+    def summary(self):
+        """Mean, min and max of each quantity over the samples in which the
+        firmware reports the graphics engine at least half busy (the table
+        lags the load by a few hundred milliseconds)."""
+        if self._smi is None:
+            return None
+        busy = [v for a, v in self.samples if a is not None and a >= 50]
+        out = {"busy_samples": len(busy), "samples": len(self.samples)}
+        for key in ("sclk_mhz", "temp_c", "power_w"):
+            v = [d[key] for d in busy if key in d]
+            if v:
+                out[key] = {"mean": round(sum(v) / len(v), 1), "min": min(v), "max": max(v)}
+        return out
+
+
+def sustained_state(step, seconds: float):
+    """Run steps back to back for about `seconds` while sampling the GPU's
+    clock, temperature and power; returns GpuMonitor.summary() (not part of
+    any timed figure)."""
+    import torch
+    if seconds <= 0:
+        return None
+    with GpuMonitor() as mon:
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < seconds:
+            for _ in range(10):
+                step()
+            torch.cuda.synchronize()
+    return mon.summary()
+
+
+def cold_steps(step, steps: int, flush_bytes: int = 512 << 20):
+    """Median time per step (ms) of `steps` single steps, each after a write
+    of `flush_bytes` (more than the L2 caches and the 256 MB MALL hold) that
+    is outside the timed events: every step starts with cold caches."""
+    import torch
+    buf = torch.empty(flush_bytes, dtype=torch.uint8, device="cuda")
+    times = []
+    for i in range(steps):
+        buf.fill_(i & 0xFF)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        step()
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+    del buf
+    times.sort()
+    return times[len(times) // 2]
+
+
 def time_steps(step, n_kernels: int, steps: int, warmup: int):
     """Run `warmup` steps, then two timed passes of `steps` steps, each after
     the GPU has been held while the host enqueues it: the first has no events
@@ -287,6 +407,7 @@ def run_paged(args, w) -> int:
 
     ms_step, kl = time_steps(step, len(kernels), args.steps, args.warmup)
     kern_ms = dict(zip(kernels, kl))
+    gpu_state = sustained_state(step, args.state_seconds)
     if not (torch.isfinite(o.float()).all() and torch.isfinite(lse).all()):
         print("non-finite output", file=sys.stderr)
         return 1
@@ -300,7 +421,8 @@ def run_paged(args, w) -> int:
            "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic (seeded i.i.d. N(0,1) bf16; seeded lengths and pages)",
-           "config": cfg, "kernel_ms": {n: round(t, 5) for n, t in kern_ms.items()}}
+           "config": cfg, "kernel_ms": {n: round(t, 5) for n, t in kern_ms.items()},
+           "gpu_state": gpu_state}
     if w.decode:
         by = decode_bytes(x)
         total = sum(by.values())
@@ -360,6 +482,7 @@ def run_gemm(args, w) -> int:
 
     attn.attn_gemm_bf16_nt(a, b, c)   # shape and pointer checks once, through the binding
     ms_step, (kern_ms,) = time_steps(step, 1, args.steps, args.warmup)
+    gpu_state = sustained_state(step, args.state_seconds)
     if not torch.isfinite(c.float()).all():
         print("non-finite output", file=sys.stderr)
         return 1
@@ -371,6 +494,7 @@ def run_gemm(args, w) -> int:
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic (seeded i.i.d. N(0,1) bf16)",
            "config": {"workload": w.name, "M": w.M, "N": w.N, "K": w.K, "seed": 0},
+           "gpu_state": gpu_state,
            "pct_peak": round(100 * F / (ms_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
            "kernel_ms": {"gemm_nt_kernel": round(kern_ms, 5)},
            "roofline": {"kernel": "gemm_nt_kernel", "bound": "mfma", "achieved": round(ach, 2),
@@ -414,6 +538,10 @@ def main(argv=None) -> int:
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
+    ap.add_argument("--cold-steps", type=int, default=10,
+                    help="steps of the cold-cache pass (0: none)")
+    ap.add_argument("--state-seconds", type=float, default=1.5,
+                    help="length of the untimed pass that samples clock, temperature and power")
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
@@ -483,6 +611,8 @@ def main(argv=None) -> int:
     kernels = ("fwd_kernel", "bwd_dq_kernel", dkdv)
     ms_step, kl = time_steps(step, len(kernels), args.steps, args.warmup)
     kern_ms = dict(zip(kernels, kl))
+    ms_cold = cold_steps(step, args.cold_steps) if args.cold_steps > 0 else None
+    gpu_state = sustained_state(step, args.state_seconds)
     for t in (o, lse, dq, dk, dv):
         if not torch.isfinite(t.float()).all():
             print("non-finite output", file=sys.stderr)
@@ -529,6 +659,12 @@ def main(argv=None) -> int:
             "traffic": load_traffic(dom, w.name),
         },
         "cpu_baseline": None,
+        "cold": None if ms_cold is None else {
+            "ms_per_step": round(ms_cold, 4),
+            "value": round(total / (ms_cold * 1e-3) / 1e12, 2),
+            "steps": args.cold_steps,
+            "note": "median step after a 512 MiB write flushes L2 and MALL (write not timed)"},
+        "gpu_state": gpu_state,
     }
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, x, args.cpu_seconds)

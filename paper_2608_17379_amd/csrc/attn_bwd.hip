@@ -9,8 +9,8 @@
 // L and return dQ, dK, dV).  Two kernels, both free of atomics:
 //
 //  * bwd_dq_kernel: one workgroup of 4 wavefronts per (segment, query head,
-//    128-row query block and its causal mirror), 32 rows per wavefront, two
-//    workgroups per CU.  Its prologue computes Delta for its rows (the rows'
+//    128-row query block; the blocks with the most key tiles first), 32 rows
+//    per wavefront, two workgroups per CU.  Its prologue computes Delta for its rows (the rows'
 //    dO and O are read once) and stores it, with L log2(e), in the
 //    workspace; the loop over key tiles recomputes S^T = K Q^T and
 //    dP^T = V dO^T, forms dS^T in registers and accumulates dQ^T += K^T dS^T.
@@ -55,9 +55,8 @@ constexpr int kTileRows = 64;
 // workgroup): the two wavefronts on a SIMD belong to different workgroups,
 // so no common barrier holds them in step, and one workgroup's prologue and
 // epilogue run under the other's loop.  K and V tiles stream through two
-// LDS stages; each wavefront takes both 32-key halves of every tile.  A
-// workgroup takes a query block and its causal mirror, so that every
-// workgroup has the same number of key tiles.
+// LDS stages; each wavefront takes both 32-key halves of every tile.  The
+// query blocks with the most key tiles under the causal mask go first.
 // ---------------------------------------------------------------------------
 constexpr int kQM = 128;   // query rows per workgroup
 constexpr int kDqWaves = 4;
@@ -90,7 +89,7 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
   const Segment seg = segment_of(L, z);
   const int nqt = (seg.len + kQM - 1) / kQM;
   const int p = (int)blockIdx.y;
-  if (p > nqt - 1 - p) return;
+  if (p >= nqt) return;
 
   // Fields used inside the lambdas below, as plain values (capturing the
   // kernel argument itself would make the compiler spill it to scratch).
@@ -104,13 +103,8 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
   const RowReader<D> rr(l32, half);
   const TransReader<D> trr(lane);
 
-#pragma nounroll
-  for (int pass = 0; pass < 2; ++pass) {
-    const int qt = pass == 0 ? nqt - 1 - p : p;
-    if (pass == 1) {
-      if (qt >= nqt - 1 - p) break;
-      __syncthreads();   // the first block's epilogue reads are done before the ring refills
-    }
+  {
+    const int qt = nqt - 1 - p;
     const int q0 = qt * kQM;
     const int64_t qoff = (int64_t)seg.start * L.q_row + (int64_t)z * L.q_batch +
                          (int64_t)h * L.q_head;
@@ -819,8 +813,8 @@ namespace {
 
 template <int D>
 void launch_bwd_d(const BwdArgs& a, int phases, hipStream_t stream) {
-  // A dQ workgroup takes a query block and its mirror (see the kernel).
-  const dim3 gq((unsigned)(a.L.nseg * a.L.Hq), (unsigned)(((a.L.S + kQM - 1) / kQM + 1) / 2));
+  // One dQ workgroup per query block (see the kernel).
+  const dim3 gq((unsigned)(a.L.nseg * a.L.Hq), (unsigned)((a.L.S + kQM - 1) / kQM));
   const dim3 gk((unsigned)(a.L.nseg * a.L.Hkv), (unsigned)((a.L.S + kKN - 1) / kKN));
   if (phases & 1) {
     if (a.causal)

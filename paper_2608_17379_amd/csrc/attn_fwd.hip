@@ -5,9 +5,9 @@
 // exp(m_old - m_new) when the maximum moves, and normalise by l in the
 // epilogue, where L = m + log l.
 //
-// Work split: one workgroup of 4 wavefronts per (segment, query head, pair of
-// 128-row query blocks), two workgroups per CU; each wavefront owns 32 query
-// rows.  The wavefront computes the transposed score tile S^T = K Q^T on
+// Work split: one workgroup of 4 wavefronts per (segment, query head,
+// 128-row query block), the blocks with the most key tiles first, two
+// workgroups per CU; each wavefront owns 32 query rows.  The wavefront computes the transposed score tile S^T = K Q^T on
 // MFMA, so lane l holds every score of query (l % 32) against half of the
 // tile's keys: the row maximum and row sum are in-lane reductions plus one
 // exchange with lane l ^ 32.  P^T, rounded to bf16, is then already laid out
@@ -67,23 +67,17 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   const Segment kseg = PAGED ? kv_segment_of(L, z) : seg;
   const int kv_len = PAGED ? min(kseg.len, a.max_kvlen) : kseg.len;
   const int dpos = PAGED ? kv_len - seg.len : 0;
-  // Unsplit: query blocks nqt - 1 - p and p of the segment, in that order:
-  // under the causal mask every workgroup then has the same number of key
-  // tiles, so the two workgroups sharing a CU finish together.  Split: query
-  // block p, key chunk blockIdx.z.
+  // Unsplit: query block nqt - 1 - p, so that the blocks with the most key
+  // tiles under the causal mask start first.  Split: query block p, key
+  // chunk blockIdx.z.
   const int nqt = (seg.len + kBM - 1) / kBM;
   const int p = (int)blockIdx.y;
   const int split = PAGED ? a.split : 0;
   const int chunk = (int)blockIdx.z;
-  if (split ? p >= nqt : p > nqt - 1 - p) return;
+  if (p >= nqt) return;
 
-#pragma nounroll
-  for (int pass = 0; pass < 2; ++pass) {
-    const int qt = split ? p : pass == 0 ? nqt - 1 - p : p;
-    if (pass == 1) {
-      if (split || qt >= nqt - 1 - p) break;
-      __syncthreads();   // the first block's last tile is read before stage 0 refills
-    }
+  {
+    const int qt = split ? p : nqt - 1 - p;
     const int q0 = qt * kBM;
     const int64_t qoff = (int64_t)seg.start * L.q_row + (int64_t)z * L.q_batch +
                          (int64_t)h * L.q_head;
@@ -436,8 +430,8 @@ hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream) {
       launch_merge<128>(a, mg, stream);
     return hipGetLastError();
   }
-  // Each workgroup takes a query block and its mirror (see the kernel).
-  const dim3 grid(heads, (unsigned)((nqt + 1) / 2));
+  // One workgroup per query block (see the kernel).
+  const dim3 grid(heads, (unsigned)nqt);
   if (a.L.kv_cu)
     launch_fwd_p<true>(a, D, grid, stream);
   else

@@ -195,8 +195,8 @@ int attn_bwd_varlen_phases(const void* q, const void* k, const void* v,
  */
 
 /* Bytes of workspace for attn_fwd_paged: 0 when the prefill runs unsplit
- * (its unsplit grid of a workgroup per pair of 128-query blocks, per request
- * and query head, fills the 256 CUs of the MI355X, or no request is longer
+ * (its unsplit grid of a workgroup per 128-query block, per request and
+ * query head, fills the 256 CUs of the MI355X, or no request is longer
  * than 256 keys), else the partial results of the 256-key chunks: fp32
  * [total_q, Hq, ceil(max_kvlen / 256), D + 1], rounded up.  The size depends
  * on the arguments alone. */

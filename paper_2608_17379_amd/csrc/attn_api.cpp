@@ -175,16 +175,16 @@ int64_t decode_chunks(int max_kvlen) {
 
 size_t round256(int64_t bytes) { return (size_t)((bytes + 255) / 256 * 256); }
 
-// A paged prefill whose unsplit grid (a workgroup per query block and its
-// causal mirror, per request and query head) has fewer workgroups than the
-// MI355X has CUs is split into chunks of keys, when its requests are longer
-// than one chunk.  The rule uses the part's CU count, not a device query, so
+// A paged prefill whose unsplit grid (a workgroup per 128-row query block,
+// per request and query head) has fewer workgroups than the MI355X has CUs
+// is split into chunks of keys, when its requests are longer than one
+// chunk.  The rule uses the part's CU count, not a device query, so
 // that the workspace size depends on the shapes alone.
 using attn::kChipCUs;
 
 int paged_split(int batch, int max_qlen, int max_kvlen, int Hq) {
   const int64_t nqt = ((int64_t)max_qlen + attn::kFwdBlockRows - 1) / attn::kFwdBlockRows;
-  const int64_t wgs = (int64_t)batch * Hq * ((nqt + 1) / 2);
+  const int64_t wgs = (int64_t)batch * Hq * nqt;
   if (max_kvlen <= attn::kFwdSplitKeys || wgs >= kChipCUs) return 0;
   return attn::kFwdSplitKeys;
 }

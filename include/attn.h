@@ -131,10 +131,11 @@ int attn_bwd_varlen(const void* q, const void* k, const void* v,
  * phases = ATTN_BWD_DQ | ATTN_BWD_DKDV is exactly attn_bwd / attn_bwd_varlen.
  * With ATTN_BWD_DKDV, one of the two bits below may be added to choose the
  * form of the dk/dv kernel at D = 96 and 128 (for tests and tuning; D = 64
- * has one form and ignores them):
+ * has only the second form and ignores them):
  *   ATTN_BWD_DKDV_ONE_PER_CU  eight wavefronts per 128 keys, one workgroup
  *                             per CU;
- *   ATTN_BWD_DKDV_TWO_PER_CU  four wavefronts per 128 keys, two per CU.
+ *   ATTN_BWD_DKDV_TWO_PER_CU  four wavefronts per 128 keys, two (at D = 64
+ *                             three) per CU.
  * Both give dk and dv equal up to the order of floating-point additions.
  * Without either the library picks two per CU, unless the mask is causal
  * and there are fewer than 1,024 blocks of 128 keys (all workgroups would
@@ -149,9 +150,9 @@ int attn_bwd_varlen(const void* q, const void* k, const void* v,
 
 /* The dk/dv form attn_bwd (packed 0: nseg = B, S the sequence length) or
  * attn_bwd_varlen (packed 1: nseg = nseq, S = max_seqlen, total) picks for
- * these arguments: ATTN_BWD_DKDV_ONE_PER_CU or ATTN_BWD_DKDV_TWO_PER_CU at
- * D = 96 and 128, 0 at D = 64 (one form); a negative status for bad
- * arguments.  No GPU call. */
+ * these arguments: ATTN_BWD_DKDV_ONE_PER_CU or ATTN_BWD_DKDV_TWO_PER_CU
+ * (always the latter at D = 64); a negative status for bad arguments.  No
+ * GPU call. */
 int attn_bwd_dkdv_form(int nseg, int Hkv, int S, int total, int D, int causal, int packed);
 int attn_bwd_phases(const void* q, const void* k, const void* v, const void* o,
                     const float* lse, const void* dO, void* dq, void* dk,

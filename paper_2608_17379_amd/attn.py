@@ -182,7 +182,7 @@ def attn_bwd(q, k, v, o, lse, dO, dq, dk, dv, causal: bool, scale: float,
 def attn_bwd_dkdv_form(nseg: int, Hkv: int, S: int, total: int, D: int, causal: bool,
                        packed: bool) -> int:
     """The dK/dV form the library picks (ATTN_BWD_DKDV_ONE_PER_CU or
-    ATTN_BWD_DKDV_TWO_PER_CU; 0 at D = 64)."""
+    ATTN_BWD_DKDV_TWO_PER_CU; always the latter at D = 64)."""
     st = lib().attn_bwd_dkdv_form(nseg, Hkv, S, total, D, int(bool(causal)), int(bool(packed)))
     if st < 0:
         _check(st, "attn_bwd_dkdv_form")

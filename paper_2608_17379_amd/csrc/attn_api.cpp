@@ -220,11 +220,9 @@ int attn_bwd_dkdv_form(int nseg, int Hkv, int S, int total, int D, int causal, i
   if (nseg < 0 || Hkv < 1 || S < 0 || total < 0) return ATTN_ERR_SHAPE;
   if (D != 64 && D != 96 && D != 128) return ATTN_ERR_HEAD_DIM;
   if ((causal != 0 && causal != 1) || (packed != 0 && packed != 1)) return ATTN_ERR_VALUE;
-  switch (attn::dkdv_form_for(nseg, Hkv, S, total, packed != 0, D, causal != 0)) {
-    case 1: return ATTN_BWD_DKDV_ONE_PER_CU;
-    case 2: return ATTN_BWD_DKDV_TWO_PER_CU;
-    default: return 0;
-  }
+  return attn::dkdv_form_for(nseg, Hkv, S, total, packed != 0, D, causal != 0) == 1
+             ? ATTN_BWD_DKDV_ONE_PER_CU
+             : ATTN_BWD_DKDV_TWO_PER_CU;
 }
 
 int attn_bwd_phases(const void* q, const void* k, const void* v, const void* o, const float* lse,

@@ -20,11 +20,10 @@
 //    or K in registers) and loops over every query head of the group and
 //    every query tile that can see its keys, accumulating dV^T += dO^T P and
 //    dK^T += Q^T dS in registers; the grouped-query sum therefore needs no
-//    cross-workgroup reduction.  At D = 128 and 96 there are two forms:
-//    bwd_dkdv_kernel with 8 wavefronts and one workgroup per CU, and
-//    bwd_dkdv4_kernel with 4 wavefronts and two per CU (chosen by the grid,
-//    see launch_bwd_d); at D = 64 bwd_dkdv_kernel has 4 wavefronts and two
-//    workgroups per CU.
+//    cross-workgroup reduction.  bwd_dkdv4_kernel has 4 wavefronts and two
+//    workgroups per CU; at D = 128 and 96, causal grids too small for two
+//    rounds of it use bwd_dkdv_kernel, with 8 wavefronts and one workgroup
+//    per CU (see dkdv_form_for).
 //
 // Tiles of 64 rows (K and V for dQ; Q, dO, L log2 e and Delta for dK/dV) go
 // from global memory straight into a ring of LDS stages (buffer_load ... lds,
@@ -282,21 +281,18 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
 // ---------------------------------------------------------------------------
 // dK, dV
 //
-// A workgroup covers 128 keys, 32 per wavefront group.  K and V of the
-// workgroup's keys stay in LDS (read as B operands) and the query-side tiles
-// (Q, dO, L log2 e, Delta) stream through two LDS stages.
-//  * D = 128 and D = 96 (rows padded to 128 elements in LDS): eight
-//    wavefronts; wavefronts w and w + 4 (which share a SIMD)
-//    own the same 32 keys and take the two 32-query halves of every 64-query
-//    tile, and their two partial dK/dV accumulators are added through LDS at
-//    the end (one workgroup per CU: 129 KiB of LDS).
-//  * D = 64: four wavefronts, each taking both halves of every tile, and two
-//    workgroups per CU (65 KiB of LDS each), so that the two wavefronts on a
-//    SIMD belong to different workgroups and are not held in step.
+// The eight-wavefront form (D = 128 and 96, rows padded to 128 elements in
+// LDS; used for causal grids too small for two rounds of the four-wavefront
+// form below).  A workgroup covers 128 keys, 32 per wavefront group.  K and
+// V of the workgroup's keys stay in LDS (read as B operands) and the
+// query-side tiles (Q, dO, L log2 e, Delta) stream through two LDS stages.
+// Wavefronts w and w + 4 (which share a SIMD) own the same 32 keys and take
+// the two 32-query halves of every 64-query tile, and their two partial
+// dK/dV accumulators are added through LDS at the end (one workgroup per
+// CU: 129 KiB of LDS).
 // ---------------------------------------------------------------------------
 constexpr int kKN = 128;        // keys per workgroup
-template <int D>
-constexpr int dkv_waves() { return D == 64 ? 4 : 8; }
+constexpr int kDkvWaves = 8;
 
 template <int D>
 struct DkvSmem {
@@ -309,16 +305,14 @@ struct DkvSmem {
   static constexpr int LSE = DO + 2 * TILE;                // 2 stages x 64 fp32
   static constexpr int DEL = LSE + 2 * 256;
   static constexpr int BYTES = DEL + 2 * 256;
-  // epilogue: one tensor's fp32 partial per wavefront (pairs), or the bf16
-  // dK and dV rows of each wavefront
-  static_assert(dkv_waves<D>() * (D / 32) * 4 * 1024 <= BYTES, "reduction buffer");
-  static_assert(dkv_waves<D>() * 2 * 32 * P * 2 <= BYTES, "epilogue staging");
+  // epilogue: one tensor's fp32 partial per wavefront
+  static_assert(kDkvWaves * (D / 32) * 4 * 1024 <= BYTES, "reduction buffer");
 };
 
 template <int D, bool CAUSAL>
-__global__ __launch_bounds__(64 * dkv_waves<D>(), D == 64 ? 2 : 1) void bwd_dkdv_kernel(BwdArgs a) {
-  constexpr int NW = dkv_waves<D>();
-  constexpr bool PAIRS = NW == 8;   // two wavefronts per key group
+__global__ __launch_bounds__(64 * kDkvWaves, 1) void bwd_dkdv_kernel(BwdArgs a) {
+  static_assert(D != 64, "D = 64 has the four-wavefront form only");
+  constexpr int NW = kDkvWaves;
   using Tile = AsyncTile<D, NW>;
   using SM = DkvSmem<D>;
   constexpr int P = SM::P;
@@ -330,7 +324,7 @@ __global__ __launch_bounds__(64 * dkv_waves<D>(), D == 64 ? 2 : 1) void bwd_dkdv
   const int lane = tid & 63, wave = wave_id();
   const int l32 = lane & 31, half = lane >> 5;
   const int kq = wave & 3;            // 32-key group
-  const int sb = PAIRS ? wave >> 2 : 0;   // query half of each tile (pairs only)
+  const int sb = wave >> 2;   // query half of each tile
 
   const Layout L = a.L;
   const int z = blockIdx.x / L.Hkv, hk = blockIdx.x % L.Hkv;
@@ -474,12 +468,7 @@ __global__ __launch_bounds__(64 * dkv_waves<D>(), D == 64 ? 2 : 1) void bwd_dkdv
     wait_vm_all();
     __syncthreads();
     if (n + 1 < niter) issue(n + 1, (n + 1) & 1);
-    if constexpr (PAIRS) {
-      compute(n, n & 1, sb, masked);
-    } else {
-      compute(n, n & 1, 0, masked);
-      compute(n, n & 1, 1, masked);
-    }
+    compute(n, n & 1, sb, masked);
   };
   const int nmask = CAUSAL ? min(2, per_head) : 0;
   issue(0, 0);
@@ -514,12 +503,7 @@ __global__ __launch_bounds__(64 * dkv_waves<D>(), D == 64 ? 2 : 1) void bwd_dkdv
       if (kw0 + row < len) st16(gout + (int64_t)(kw0 + row) * kv_row + 8 * ch, v);
     }
   };
-  if constexpr (!PAIRS) {
-    // Each wavefront holds the whole of its keys' dK and dV.
-    uint16_t* stg = reinterpret_cast<uint16_t*>(smem) + wave * 2 * 32 * P;
-    store_rows(dkacc, a.scale, stg, a.dk + kvoff);
-    store_rows(dvacc, 1.f, stg + 32 * P, a.dv + kvoff);
-  } else {
+  {
     // The pair splits the work: the sb = 0 wavefront finalises dK, the
     // sb = 1 one dV.  Each first hands its partial of the other tensor to
     // its partner, then adds the partner's partial to its own.
@@ -560,8 +544,9 @@ __global__ __launch_bounds__(64 * dkv_waves<D>(), D == 64 ? 2 : 1) void bwd_dkdv
 }
 
 // ---------------------------------------------------------------------------
-// dK, dV at D = 128 and D = 96: four wavefronts per 128 keys, two workgroups
-// per CU.  Each wavefront owns 32 keys outright (no partial to combine): its
+// dK, dV, four-wavefront form (every D; the only form at D = 64): four
+// wavefronts per 128 keys, two workgroups per CU (three at D = 64, whose
+// registers allow it).  Each wavefront owns 32 keys outright (no partial to combine): its
 // K rows stay in registers as the B operand of S = Q K^T, the workgroup's V
 // rows in LDS (B operand of dP = dO V^T), and the query side streams through
 // two LDS stages of 32 rows.  64.5 KiB of LDS per workgroup, so the two
@@ -796,12 +781,12 @@ template __global__ void bwd_dq_kernel<96, false>(BwdArgs);
 template __global__ void bwd_dq_kernel<96, true>(BwdArgs);
 template __global__ void bwd_dq_kernel<128, false>(BwdArgs);
 template __global__ void bwd_dq_kernel<128, true>(BwdArgs);
-template __global__ void bwd_dkdv_kernel<64, false>(BwdArgs);
-template __global__ void bwd_dkdv_kernel<64, true>(BwdArgs);
 template __global__ void bwd_dkdv_kernel<96, false>(BwdArgs);
 template __global__ void bwd_dkdv_kernel<96, true>(BwdArgs);
 template __global__ void bwd_dkdv_kernel<128, false>(BwdArgs);
 template __global__ void bwd_dkdv_kernel<128, true>(BwdArgs);
+template __global__ void bwd_dkdv4_kernel<64, false>(BwdArgs);
+template __global__ void bwd_dkdv4_kernel<64, true>(BwdArgs);
 template __global__ void bwd_dkdv4_kernel<96, false>(BwdArgs);
 template __global__ void bwd_dkdv4_kernel<96, true>(BwdArgs);
 template __global__ void bwd_dkdv4_kernel<128, false>(BwdArgs);
@@ -823,22 +808,23 @@ void launch_bwd_d(const BwdArgs& a, int phases, hipStream_t stream) {
       hipLaunchKernelGGL((bwd_dq_kernel<D, false>), gq, dim3(kDqThreads), 0, stream, a);
   }
   if (phases & 2) {
-    if constexpr (D != 64) {
-      const int form = a.dkdv_form ? a.dkdv_form
+    const int form = D == 64 ? 2
+                     : a.dkdv_form ? a.dkdv_form
                                    : dkdv_form_for(a.L.nseg, a.L.Hkv, a.L.S, a.L.total,
                                                    a.L.cu != nullptr, D, a.causal != 0);
-      if (form == 2) {
-        if (a.causal)
-          hipLaunchKernelGGL((bwd_dkdv4_kernel<D, true>), gk, dim3(256), 0, stream, a);
-        else
-          hipLaunchKernelGGL((bwd_dkdv4_kernel<D, false>), gk, dim3(256), 0, stream, a);
-        return;
-      }
+    if (form == 2) {
+      if (a.causal)
+        hipLaunchKernelGGL((bwd_dkdv4_kernel<D, true>), gk, dim3(256), 0, stream, a);
+      else
+        hipLaunchKernelGGL((bwd_dkdv4_kernel<D, false>), gk, dim3(256), 0, stream, a);
+      return;
     }
-    if (a.causal)
-      hipLaunchKernelGGL((bwd_dkdv_kernel<D, true>), gk, dim3(64 * dkv_waves<D>()), 0, stream, a);
-    else
-      hipLaunchKernelGGL((bwd_dkdv_kernel<D, false>), gk, dim3(64 * dkv_waves<D>()), 0, stream, a);
+    if constexpr (D != 64) {
+      if (a.causal)
+        hipLaunchKernelGGL((bwd_dkdv_kernel<D, true>), gk, dim3(64 * kDkvWaves), 0, stream, a);
+      else
+        hipLaunchKernelGGL((bwd_dkdv_kernel<D, false>), gk, dim3(64 * kDkvWaves), 0, stream, a);
+    }
   }
 }
 
@@ -850,7 +836,7 @@ void launch_bwd_d(const BwdArgs& a, int phases, hipStream_t stream) {
 // one-per-CU form.  Packed layouts count their sequences' blocks, about
 // total / 128 + nseq per key head.
 int dkdv_form_for(int nseg, int Hkv, int S, int total, bool packed, int D, bool causal) {
-  if (D == 64) return 0;
+  if (D == 64) return 2;   // the four-wavefront form is the only one at D = 64
   const int64_t blocks = packed ? (int64_t)Hkv * (total / kKN + nseg)
                                 : (int64_t)nseg * Hkv * ((S + kKN - 1) / kKN);
   return !causal || blocks >= 4 * kChipCUs ? 2 : 1;

@@ -118,8 +118,9 @@ constexpr int kFwdBlockRows = 128;   // query rows per forward workgroup
 hipError_t launch_decode(const DecodeArgs& a, int D, int phases, hipStream_t stream);
 // phases: bit 0 = Delta and dQ kernel, bit 1 = dK/dV kernel.
 hipError_t launch_bwd(const BwdArgs& a, int D, int phases, hipStream_t stream);
-// The dK/dV form launch_bwd picks when BwdArgs::dkdv_form is 0: 1 (one
-// workgroup per CU) or 2 (two per CU) at D = 96 and 128, 0 at D = 64.
+// The dK/dV form launch_bwd picks when BwdArgs::dkdv_form is 0: 1 (eight
+// wavefronts, one workgroup per CU) or 2 (four wavefronts, two per CU);
+// always 2 at D = 64.
 int dkdv_form_for(int nseg, int Hkv, int S, int total, bool packed, int D, bool causal);
 
 }  // namespace attn

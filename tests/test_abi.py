@@ -265,7 +265,8 @@ def test_dkdv_form_rule():
     assert form(2, 8, 4096, 0, 128, False, False) == two      # non-causal blocks are equal
     assert form(1, 16, 16384, 0, 96, True, False) == two
     assert form(33, 4, 1500, 16294, 128, True, True) == one   # ~640 packed blocks
-    assert form(4, 48, 4096, 0, 64, True, False) == 0         # D = 64: one form
+    assert form(4, 48, 4096, 0, 64, True, False) == two       # D = 64: one form
+    assert form(2, 8, 4096, 0, 64, True, False) == two
     l = attn.lib()
     assert l.attn_bwd_dkdv_form(1, 1, 128, 0, 80, 1, 0) == -4
     assert l.attn_bwd_dkdv_form(-1, 1, 128, 0, 128, 1, 0) == -2

@@ -67,7 +67,7 @@ FORMS = [attn.ATTN_BWD_DKDV_ONE_PER_CU, attn.ATTN_BWD_DKDV_TWO_PER_CU]
 
 
 @pytest.mark.parametrize("form", FORMS)
-@pytest.mark.parametrize("D", [96, 128])
+@pytest.mark.parametrize("D", [64, 96, 128])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("S", [17, 65, 129, 383])
 def test_dkdv_forms(S, causal, D, form):
@@ -100,7 +100,7 @@ def test_dkdv_phase_repeated_after_one_dq_phase():
 
 
 @pytest.mark.parametrize("form", FORMS)
-@pytest.mark.parametrize("D", [96, 128])
+@pytest.mark.parametrize("D", [64, 96, 128])
 def test_dkdv_forms_gqa_and_packed(D, form):
     _fixed_case(190, D, True, Hq=8, Hkv=2, B=2, dkdv_form=form)
     w = wl.small(f"varlen_forms_d{D}", 6, 4, 1, 300, D, True, varlen=True)

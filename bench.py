@@ -14,12 +14,17 @@ GEMM workload's step is one attn_gemm_bf16_nt call (2 M N K FLOP).
 
 A step is one forward (attn_fwd) and one backward (attn_bwd_phases with the
 Delta/dQ phase, then the dK/dV phase: together exactly attn_bwd) over one
-batch of seeded synthetic bf16 inputs already resident in HBM.  W untimed
-steps, then K timed steps between two synchronisations; one JSON line is
-printed.  Before the timed steps the GPU runs a spin kernel long enough for
-the host to enqueue all K steps, so the steps run back to back and the
-timing is the GPU's, not the host's launch rate.  The K timed steps carry no
-events inside them; a second pass of K steps, not part of `value`, records
+batch of seeded synthetic bf16 inputs already resident in HBM.  At least W
+untimed warm-up steps run back to back, and more until --warmup-seconds
+(default 1 s) have passed, because the GPU's clock and power management take
+about a second of sustained load to settle (the JSON's "warmup" is the count
+actually run); then K timed steps between two synchronisations; one JSON
+line is printed.  When the host cannot enqueue steps faster than the GPU
+runs them (the microsecond-scale paged and small workloads), the GPU first
+runs a spin kernel long enough for the host to enqueue all K steps, so that
+they run back to back and the timing is the GPU's, not the host's launch
+rate; otherwise the timed steps follow the warm-up directly.  The K timed
+steps carry no events inside them; a second pass of K steps, not part of `value`, records
 an event around every launch for the per-kernel times.
 
 Two secondary objects: "cold" (fwd+bwd workloads) is the median of
@@ -281,37 +286,59 @@ def cold_steps(step, steps: int, flush_bytes: int = 512 << 20):
     return times[len(times) // 2]
 
 
-def time_steps(step, n_kernels: int, steps: int, warmup: int):
-    """Run `warmup` steps, then two timed passes of `steps` steps, each after
-    the GPU has been held while the host enqueues it: the first has no events
-    inside the steps (its time per step is the reported one), the second
-    records an event around every launch (per-kernel times).  `step(ev)`
-    records ev[0] before its first launch and ev[1 + i] after launch i.
-    Returns (ms per step, [ms per launch i])."""
+def time_steps(step, n_kernels: int, steps: int, warmup: int, warmup_seconds: float = 1.0):
+    """Warm up, then run two timed passes of `steps` steps: the first has no
+    events inside the steps (its time per step is the reported one), the
+    second records an event around every launch (per-kernel times).
+    `step(ev)` records ev[0] before its first launch and ev[1 + i] after
+    launch i.
+
+    Warm-up: `warmup` steps, then more back-to-back steps until
+    `warmup_seconds` have passed: the GPU's clock and power management take
+    about a second of sustained load to settle, and steps timed earlier run
+    up to 12 % slower.  If the host enqueues a step in less than half the
+    time the GPU takes to run it, the timed passes follow the warm-up
+    directly (the queue stays full); otherwise the GPU is first held by a
+    spin kernel while the host enqueues the pass, so that the timing is the
+    GPU's and not the host's launch rate.
+    Returns (ms per step, [ms per launch i], warm-up steps run)."""
     import torch
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_kernels + 1)]
-           for _ in range(max(steps, warmup, 1))]
+           for _ in range(max(steps, 1))]
+    # Host enqueue rate against GPU rate, on a few steps that cannot fill the
+    # launch queue (once it is full, enqueueing waits for the GPU).
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(warmup):
-        step(evs[i])
-    host_ms = (time.perf_counter() - t0) * 1e3 / max(1, warmup)
+    probe = 5
+    for _ in range(probe):
+        step()
+    host_ms = (time.perf_counter() - t0) * 1e3 / probe
+    torch.cuda.synchronize()
+    gpu_ms = (time.perf_counter() - t0) * 1e3 / probe
+    hold = host_ms >= 0.5 * gpu_ms
+    done = probe
+    t0 = time.perf_counter()
+    while done < warmup or time.perf_counter() - t0 < warmup_seconds:
+        step()
+        done += 1
     torch.cuda.synchronize()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    hold_gpu_for_enqueue(host_ms, steps)
+    if hold:
+        hold_gpu_for_enqueue(host_ms, steps)
     start.record()
     for _ in range(steps):
         step()
     end.record()
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(end) / steps
-    hold_gpu_for_enqueue(host_ms, steps)
+    if hold:
+        hold_gpu_for_enqueue(host_ms, steps)
     for i in range(steps):
         step(evs[i])
     torch.cuda.synchronize()
     kern = [sum(e[j].elapsed_time(e[j + 1]) for e in evs[:steps]) / steps
             for j in range(n_kernels)]
-    return ms_step, kern
+    return ms_step, kern, done
 
 
 # ---------------------------------------------------------------------------
@@ -405,7 +432,8 @@ def run_paged(args, w) -> int:
             if ev is not None:
                 ev[1 + i].record()
 
-    ms_step, kl = time_steps(step, len(kernels), args.steps, args.warmup)
+    ms_step, kl, warmed = time_steps(step, len(kernels), args.steps, args.warmup,
+                                     args.warmup_seconds)
     kern_ms = dict(zip(kernels, kl))
     gpu_state = sustained_state(step, args.state_seconds)
     if not (torch.isfinite(o.float()).all() and torch.isfinite(lse).all()):
@@ -417,7 +445,7 @@ def run_paged(args, w) -> int:
            "nnz": w.nnz, "num_pages": w.num_pages, "page_size": 1, "causal": w.causal,
            "decode": w.decode, "seed": 0,
            "kv_lens": [b - a for a, b in zip(x.kv_indptr, x.kv_indptr[1:])]}
-    rec = {"n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+    rec = {"n_gpus": 1, "steps": args.steps, "warmup": warmed,
            "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic (seeded i.i.d. N(0,1) bf16; seeded lengths and pages)",
@@ -481,7 +509,8 @@ def run_gemm(args, w) -> int:
             ev[1].record()
 
     attn.attn_gemm_bf16_nt(a, b, c)   # shape and pointer checks once, through the binding
-    ms_step, (kern_ms,) = time_steps(step, 1, args.steps, args.warmup)
+    ms_step, (kern_ms,), warmed = time_steps(step, 1, args.steps, args.warmup,
+                                             args.warmup_seconds)
     gpu_state = sustained_state(step, args.state_seconds)
     if not torch.isfinite(c.float()).all():
         print("non-finite output", file=sys.stderr)
@@ -490,7 +519,7 @@ def run_gemm(args, w) -> int:
     ach = F / (kern_ms * 1e-3) / 1e12
     rec = {"metric": f"bf16 GEMM TFLOP/s, {w.name}",
            "value": round(F / (ms_step * 1e-3) / 1e12, 2), "unit": "TFLOP/s", "n_gpus": 1,
-           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 5),
+           "steps": args.steps, "warmup": warmed, "ms_per_step": round(ms_step, 5),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic (seeded i.i.d. N(0,1) bf16)",
            "config": {"workload": w.name, "M": w.M, "N": w.N, "K": w.K, "seed": 0},
@@ -533,7 +562,10 @@ def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=10,
+                    help="minimum untimed warm-up steps (more run until --warmup-seconds)")
+    ap.add_argument("--warmup-seconds", type=float, default=1.0,
+                    help="minimum length of the warm-up (the GPU's clocks settle under load)")
     ap.add_argument("--workload", default=None)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -609,7 +641,8 @@ def main(argv=None) -> int:
                                    q.shape[0] if w.varlen else 0, w.D, w.causal, w.varlen)
     dkdv = "bwd_dkdv4_kernel" if form == attn.ATTN_BWD_DKDV_TWO_PER_CU else "bwd_dkdv_kernel"
     kernels = ("fwd_kernel", "bwd_dq_kernel", dkdv)
-    ms_step, kl = time_steps(step, len(kernels), args.steps, args.warmup)
+    ms_step, kl, warmed = time_steps(step, len(kernels), args.steps, args.warmup,
+                                     args.warmup_seconds)
     kern_ms = dict(zip(kernels, kl))
     ms_cold = cold_steps(step, args.cold_steps) if args.cold_steps > 0 else None
     gpu_state = sustained_state(step, args.state_seconds)
@@ -635,7 +668,7 @@ def main(argv=None) -> int:
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": args.warmup,
+        "warmup": warmed,
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True,
         "scaling": "weak",

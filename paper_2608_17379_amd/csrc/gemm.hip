@@ -5,7 +5,8 @@
 // One workgroup of 8 wavefronts per 256 x 256 tile of C, one workgroup per
 // CU.  Each K step of 64 copies the A and B tiles (256 rows x 128 bytes
 // each) straight from global memory into a two-stage LDS ring
-// (buffer_load ... lds, issued a step ahead), in the swizzled row-major
+// (buffer_load ... lds, issued a step ahead and spread over the step's K
+// chunks), in the swizzled row-major
 // layout of the attention kernels, so that every MFMA operand is one
 // conflict-free 16-byte LDS read.  Wavefront (wm, wn) owns rows
 // 128 wm .. + 127 of the tile and columns 64 wn .. + 63, as 4 x 2 blocks of
@@ -40,6 +41,7 @@ constexpr int kBand = 4;   // row tiles per band of the tile order
 
 using GTile = AsyncTile<64, kWaves>;   // one [64 rows][64 k] sub-tile per DMA instruction
 static_assert(GTile::NJ == 1, "one DMA instruction per wavefront per 64-row sub-tile");
+static_assert(kTK / 16 == 4, "one 64-row sub-tile copied per 16-wide K chunk");
 constexpr int kSubElems = GTile::ELEMS;            // 4096 bf16
 constexpr int kTileElems = 4 * kSubElems;          // 256 rows
 
@@ -81,18 +83,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs g) {
   const int lg = GTile::chunk_of(wave, 0, lane);
   const int doff = drow * row_bytes + 16 * lg;
 
-  auto load = [&](int kt, uint16_t* da, uint16_t* db) __attribute__((always_inline)) {
+  // Copies of 64-row sub-tile s of step kt (A, when the tile has it, and B).
+  auto load_part = [&](int kt, int s, uint16_t* da, uint16_t* db) __attribute__((always_inline)) {
     const int k0 = kt * kTK;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      int off = doff + 64 * s * row_bytes + 2 * k0;
-      if constexpr (KTAIL) off = k0 + 8 * lg < K ? off : kPadOffset;
-      if (s < ASUB)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            ra, (ATTN_LDS void*)(da + s * kSubElems + wave * 64 * 8), 16, off, 0, 0, 0);
+    int off = doff + 64 * s * row_bytes + 2 * k0;
+    if constexpr (KTAIL) off = k0 + 8 * lg < K ? off : kPadOffset;
+    if (s < ASUB)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rb, (ATTN_LDS void*)(db + s * kSubElems + wave * 64 * 8), 16, off, 0, 0, 0);
-    }
+          ra, (ATTN_LDS void*)(da + s * kSubElems + wave * 64 * 8), 16, off, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rb, (ATTN_LDS void*)(db + s * kSubElems + wave * 64 * 8), 16, off, 0, 0, 0);
   };
 
   const int wm = wave >> 2, wn = wave & 3;   // rows (TM / 2) wm .., columns 64 wn ..
@@ -107,7 +107,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
 
-  auto compute = [&](const uint16_t* sa, const uint16_t* sb) __attribute__((always_inline)) {
+  // One step's products on stage (sa, sb).  When `next` is set, the copies
+  // of step kt_next into (na, nb) are spread over the step, one sub-tile per
+  // 16-wide K chunk, instead of leaving in one burst.
+  auto compute = [&](const uint16_t* sa, const uint16_t* sb, bool next, int kt_next, uint16_t* na,
+                     uint16_t* nb) __attribute__((always_inline)) {
 #pragma unroll
     for (int c = 0; c < kTK / 16; ++c) {
       u32x4 bo[NB], ao[MB];
@@ -115,6 +119,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs g) {
       for (int j = 0; j < NB; ++j) bo[j] = ld16(sb + (NB * wn + j) * 2048 + rr.rm[c]);
 #pragma unroll
       for (int i = 0; i < MB; ++i) ao[i] = ld16(sa + (MB * wm + i) * 2048 + rr.rm[c]);
+      if (next) load_part(kt_next, c, na, nb);
 #pragma unroll
       for (int j = 0; j < NB; ++j)
 #pragma unroll
@@ -124,16 +129,18 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs g) {
 
   const int nkt = (K + kTK - 1) / kTK;
   // Step kt: wait for its copies (this wavefront's, then everyone's through
-  // the barrier, which also frees the stage read at kt - 1), start the copies
-  // of kt + 1 into that stage, then compute.
+  // the barrier, which also frees the stage read at kt - 1), then compute,
+  // copying kt + 1 into that stage along the way.
   auto step = [&](int kt, const uint16_t* ca, const uint16_t* cb, uint16_t* na, uint16_t* nb)
       __attribute__((always_inline)) {
     wait_vm<0>();
     __syncthreads();
-    if (kt + 1 < nkt) load(kt + 1, na, nb);
-    compute(ca, cb);
+    compute(ca, cb, kt + 1 < nkt, kt + 1, na, nb);
   };
-  if (nkt > 0) load(0, sa0, sb0);
+  if (nkt > 0) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) load_part(0, s, sa0, sb0);
+  }
   int kt = 0;
   for (; kt + 1 < nkt; kt += 2) {
     step(kt, sa0, sb0, sa1, sb1);

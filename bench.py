@@ -18,7 +18,7 @@ batch of seeded synthetic bf16 inputs already resident in HBM.  At least W
 untimed warm-up steps run back to back, and more until --warmup-seconds
 (default 1 s) have passed, because the GPU's clock and power management take
 about a second of sustained load to settle (the JSON's "warmup" is the count
-actually run); then K timed steps between two synchronisations; one JSON
+actually run, "warmup_requested" the W asked for); then K timed steps between two synchronisations; one JSON
 line is printed.  When the host cannot enqueue steps faster than the GPU
 runs them (the microsecond-scale paged and small workloads), the GPU first
 runs a spin kernel long enough for the host to enqueue all K steps, so that
@@ -445,7 +445,8 @@ def run_paged(args, w) -> int:
            "nnz": w.nnz, "num_pages": w.num_pages, "page_size": 1, "causal": w.causal,
            "decode": w.decode, "seed": 0,
            "kv_lens": [b - a for a, b in zip(x.kv_indptr, x.kv_indptr[1:])]}
-    rec = {"n_gpus": 1, "steps": args.steps, "warmup": warmed,
+    rec = {"n_gpus": 1, "steps": args.steps, "warmup": warmed, "warmup_requested": args.warmup,
+           "warmup_seconds": args.warmup_seconds,
            "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic (seeded i.i.d. N(0,1) bf16; seeded lengths and pages)",
@@ -519,7 +520,8 @@ def run_gemm(args, w) -> int:
     ach = F / (kern_ms * 1e-3) / 1e12
     rec = {"metric": f"bf16 GEMM TFLOP/s, {w.name}",
            "value": round(F / (ms_step * 1e-3) / 1e12, 2), "unit": "TFLOP/s", "n_gpus": 1,
-           "steps": args.steps, "warmup": warmed, "ms_per_step": round(ms_step, 5),
+           "steps": args.steps, "warmup": warmed, "warmup_requested": args.warmup,
+           "warmup_seconds": args.warmup_seconds, "ms_per_step": round(ms_step, 5),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic (seeded i.i.d. N(0,1) bf16)",
            "config": {"workload": w.name, "M": w.M, "N": w.N, "K": w.K, "seed": 0},
@@ -668,7 +670,8 @@ def main(argv=None) -> int:
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": warmed,
+        "warmup": warmed, "warmup_requested": args.warmup,
+        "warmup_seconds": args.warmup_seconds,
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True,
         "scaling": "weak",

@@ -25,8 +25,9 @@
 //    rounds of it use bwd_dkdv_kernel, with 8 wavefronts and one workgroup
 //    per CU (see dkdv_form_for).
 //
-// Tiles of 64 rows (K and V for dQ; Q, dO, L log2 e and Delta for dK/dV) go
-// from global memory straight into a ring of LDS stages (buffer_load ... lds,
+// Tiles of 64 rows (K and V for dQ; Q, dO, L log2 e and Delta for dK/dV, in
+// 32-row steps for bwd_dkdv4_kernel) go from global memory straight into a
+// ring of LDS stages (buffer_load ... lds,
 // bounded at the segment end so that rows past it read as zero), issued a
 // tile ahead with one barrier per tile.  They stay row-major in LDS: operands
 // whose reduction index runs along the tile's rows (K^T, Q^T, dO^T) come out

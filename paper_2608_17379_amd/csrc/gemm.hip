@@ -119,7 +119,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs g) {
       for (int j = 0; j < NB; ++j) bo[j] = ld16(sb + (NB * wn + j) * 2048 + rr.rm[c]);
 #pragma unroll
       for (int i = 0; i < MB; ++i) ao[i] = ld16(sa + (MB * wm + i) * 2048 + rr.rm[c]);
-      if (next) load_part(kt_next, c, na, nb);
+      // The copies go out at raised wave priority, ahead of the other
+      // wavefront's MFMA and LDS issue on the SIMD, so that they have as much
+      // of the step as possible to land.
+      if (next) {
+        __builtin_amdgcn_s_setprio(3);
+        load_part(kt_next, c, na, nb);
+        __builtin_amdgcn_s_setprio(0);
+      }
 #pragma unroll
       for (int j = 0; j < NB; ++j)
 #pragma unroll

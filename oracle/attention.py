@@ -31,6 +31,9 @@ The arithmetic is the textbook one, in fp64:
 Query rows are independent in this definition, so rows are processed in
 blocks of at most ``block_rows`` purely to bound the fp64 temporaries; each
 block still sees whole key rows (two-pass softmax, no online rescaling).
+Under the causal mask a block's scores stop at the last key any of its rows
+can see: the keys after it are masked for every row of the block, so they
+would only contribute exact zeros to P, O and the gradients.
 """
 from __future__ import annotations
 
@@ -49,11 +52,11 @@ def _as64(x: torch.Tensor) -> torch.Tensor:
 def _scores(qb: torch.Tensor, kh: torch.Tensor, row0: int, causal: bool,
             scale: float) -> torch.Tensor:
     """X = scale * Q_I K^T for the query rows I = row0 .. row0+len(qb)-1."""
-    x = scale * (qb @ kh.transpose(0, 1))
+    x = (qb @ kh.transpose(0, 1)).mul_(scale)
     if causal:
         rows = torch.arange(row0, row0 + qb.shape[0]).unsqueeze(1)
         cols = torch.arange(kh.shape[0]).unsqueeze(0)
-        x = x.masked_fill(cols > rows, -math.inf)
+        x.masked_fill_(cols > rows, -math.inf)
     return x
 
 
@@ -63,11 +66,18 @@ def _softmax_rows(x: torch.Tensor):
     # A row with every entry masked has m = -inf; it gets P = 0 and L = -inf.
     empty = torch.isinf(m) & (m < 0)
     m_safe = torch.where(empty, torch.zeros_like(m), m)
-    e = torch.exp(x - m_safe)
+    e = (x - m_safe).exp_()   # 0 wherever x is -inf, so on every entry of an empty row
     l = e.sum(dim=1, keepdim=True)
-    p = torch.where(empty, torch.zeros_like(e), e / torch.where(empty, torch.ones_like(l), l))
+    p = e.div_(torch.where(empty, torch.ones_like(l), l))
     lse = torch.where(empty, torch.full_like(m, -math.inf), m_safe + torch.log(l))
     return p, lse.squeeze(1)
+
+
+def _visible_keys(nkeys: int, last_pos: int, causal: bool) -> int:
+    """Number of leading keys a block of query rows can see: under the causal
+    mask no row at a position <= last_pos sees key last_pos + 1 or later, and
+    such keys would only add exact zeros to P, so they are left out."""
+    return max(0, min(nkeys, last_pos + 1)) if causal else nkeys
 
 
 def _head_forward(qh, kh, vh, causal, scale, block_rows, pos0=0):
@@ -76,12 +86,13 @@ def _head_forward(qh, kh, vh, causal, scale, block_rows, pos0=0):
     n = qh.shape[0]
     o = torch.zeros(n, vh.shape[1], dtype=_F64)
     lse = torch.full((n,), -math.inf, dtype=_F64)
-    if kh.shape[0] == 0:   # no keys at all: every row is empty
-        return o, lse
     for r0 in range(0, n, block_rows):
         r1 = min(n, r0 + block_rows)
-        p, l = _softmax_rows(_scores(qh[r0:r1], kh, pos0 + r0, causal, scale))
-        o[r0:r1] = p @ vh
+        kend = _visible_keys(kh.shape[0], pos0 + r1 - 1, causal)
+        if kend == 0:   # no row of the block sees a key: O = 0, L = -inf
+            continue
+        p, l = _softmax_rows(_scores(qh[r0:r1], kh[:kend], pos0 + r0, causal, scale))
+        o[r0:r1] = p @ vh[:kend]
         lse[r0:r1] = l
     return o, lse
 
@@ -94,13 +105,17 @@ def _head_backward(qh, kh, vh, doh, causal, scale, block_rows):
     dv = torch.zeros_like(vh)
     for r0 in range(0, n, block_rows):
         r1 = min(n, r0 + block_rows)
-        p, _ = _softmax_rows(_scores(qh[r0:r1], kh, r0, causal, scale))
-        dp = doh[r0:r1] @ vh.transpose(0, 1)
+        kend = _visible_keys(kh.shape[0], r1 - 1, causal)
+        if kend == 0:
+            continue
+        kb, vb = kh[:kend], vh[:kend]
+        p, _ = _softmax_rows(_scores(qh[r0:r1], kb, r0, causal, scale))
+        dp = doh[r0:r1] @ vb.transpose(0, 1)
         delta = (p * dp).sum(dim=1, keepdim=True)
-        ds = p * (dp - delta)
-        dq[r0:r1] = scale * (ds @ kh)
-        dk += scale * (ds.transpose(0, 1) @ qh[r0:r1])
-        dv += p.transpose(0, 1) @ doh[r0:r1]
+        ds = dp.sub_(delta).mul_(p)   # dS = P * (dP - Delta)
+        dq[r0:r1] = scale * (ds @ kb)
+        dk[:kend] += scale * (ds.transpose(0, 1) @ qh[r0:r1])
+        dv[:kend] += p.transpose(0, 1) @ doh[r0:r1]
     return dq, dk, dv
 
 

@@ -14,18 +14,23 @@ GEMM workload's step is one attn_gemm_bf16_nt call (2 M N K FLOP).
 
 A step is one forward (attn_fwd) and one backward (attn_bwd_phases with the
 Delta/dQ phase, then the dK/dV phase: together exactly attn_bwd) over one
-batch of seeded synthetic bf16 inputs already resident in HBM.  At least W
-untimed warm-up steps run back to back, and more until --warmup-seconds
-(default 1 s) have passed, because the GPU's clock and power management take
-about a second of sustained load to settle (the JSON's "warmup" is the count
-actually run, "warmup_requested" the W asked for); then K timed steps between two synchronisations; one JSON
-line is printed.  When the host cannot enqueue steps faster than the GPU
-runs them (the microsecond-scale paged and small workloads), the GPU first
-runs a spin kernel long enough for the host to enqueue all K steps, so that
-they run back to back and the timing is the GPU's, not the host's launch
-rate; otherwise the timed steps follow the warm-up directly.  The K timed
-steps carry no events inside them; a second pass of K steps, not part of `value`, records
-an event around every launch for the per-kernel times.
+batch of seeded synthetic bf16 inputs already resident in HBM.  After a
+five-step probe and W untimed warm-up steps, K steps are timed
+("at_requested_warmup", the paper's fixed warm-up count); more back-to-back
+steps then run until --warmup-seconds (default 1 s) have passed since the
+probe, because the GPU's clock and power management take about a second of
+sustained load to settle, and K more steps are timed: that pass is `value`
+(the JSON's "warmup" is the count run before it, "warmup_requested" the W
+asked for).  "median" is the median per-step time of a further pass with an
+event between consecutive steps.  When the host cannot enqueue steps faster
+than the GPU runs them (the microsecond-scale paged and small workloads),
+the GPU first runs a spin kernel long enough for the host to enqueue all K
+steps of a pass, so that they run back to back and the timing is the GPU's,
+not the host's launch rate; otherwise a pass's start event is recorded
+behind the steps before it, with the launch queue still full.  The timed
+passes carry no events inside their steps; a last pass of K steps, not part
+of `value`, records an event around every launch for the per-kernel times.
+One JSON line is printed.
 
 Two secondary objects: "cold" (fwd+bwd workloads) is the median of
 --cold-steps single steps, each started after a 512 MiB write has flushed the
@@ -41,21 +46,30 @@ x 4096 FLOP/clock/CU).
 
 The roofline object is for the kernel with the largest average duration.
 Each kernel's average duration comes from HIP events recorded between the
-launches of the second pass (all on the stream the library launches on).
-Per-launch algorithmic FLOP of each kernel:
+launches of the last pass (all on the stream the library launches on).  Its
+bound is the roof the kernel's algorithmic work meets first: the MFMA roof
+(FLOP / 2516.6 TFLOP/s) or the HBM roof (algorithmic bytes / 8 TB/s, every
+input read and every output written once); `achieved` is that work per
+second and `frac` its fraction of the roof.
+Per-launch algorithmic FLOP of each kernel (the backward's 2.5 F are its
+five S^2 D products: the recomputed S, dP, dV, dK and dQ):
   fwd_kernel       2 GEMMs  (S = QK^T, O = PV)            = F
-  bwd_dq_kernel    3 GEMMs  (S, dP = dO V^T, dQ = dS K)   = 1.5 F
-  dK/dV kernel     4 GEMMs  (S, dP, dV = P^T dO, dK)      = 2 F
+  dK/dV kernel     4 GEMMs  (S, dP = dO V^T, dV = P^T dO, dK = dS^T Q) = 2 F
                    (bwd_dkdv4_kernel or bwd_dkdv_kernel, the form the library
                    picks for the workload, attn_bwd_dkdv_form)
-with F the forward FLOP above.  `traffic` (HBM bytes per launch from
+  bwd_dq_kernel    1 GEMM   (dQ = dS K)                   = 0.5 F
+with F the forward FLOP above.  The dQ kernel also recomputes S and dP (it
+executes 3 GEMMs, 1.5 F, of MFMA work); "kernel_tflops" gives each kernel's
+algorithmic and executed rates.  `traffic` (HBM bytes per launch from
 rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a copy-kernel calibration) is
 read from profiles/traffic.json when that file was taken on the current
 kernel source (comments aside), else null.
 
 The CPU baseline times the fp64 oracle (test infrastructure, used here only
 for this leg) on a bounded sample of the same workload: whole (batch, head)
-slices, forward + backward, until about --cpu-seconds have elapsed.
+slices, forward + backward, until about --cpu-seconds have elapsed, on every
+usable host thread (the CPU affinity, capped by OMP_NUM_THREADS when set),
+with the thread count and the CPU model in the record.
 """
 from __future__ import annotations
 
@@ -73,7 +87,12 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2516.6
 PEAK_HBM_GBS = 8000.0
 METRIC = "attention fwd/bwd TFLOP/s + % bf16 MFMA peak, B4 H16 S2048 D128 causal"
-GEMMS = {"fwd_kernel": 2, "bwd_dq_kernel": 3, "bwd_dkdv_kernel": 4, "bwd_dkdv4_kernel": 4}
+# S^2 D products per launch (each 2 S^2 D FLOP per head, halved when causal):
+# algorithmic (the FLOP convention) and executed (MFMA work actually issued).
+GEMMS = {"fwd_kernel": 2, "bwd_dq_kernel": 1, "bwd_dkdv_kernel": 4, "bwd_dkdv4_kernel": 4}
+GEMMS_EXECUTED = {"fwd_kernel": 2, "bwd_dq_kernel": 3, "bwd_dkdv_kernel": 4,
+                  "bwd_dkdv4_kernel": 4}
+RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # FLOP per byte at both roofs
 KERNEL_SOURCES = {"fwd_kernel": "attn_fwd.hip", "fwd_kernel+fwd_merge_kernel": "attn_fwd.hip",
                   "bwd_dq_kernel": "attn_bwd.hip",
                   "bwd_dkdv_kernel": "attn_bwd.hip", "bwd_dkdv4_kernel": "attn_bwd.hip",
@@ -91,15 +110,38 @@ def fwd_flops(w, cu_seqlens=None) -> float:
     return f * (0.5 if w.causal else 1.0)
 
 
+def kernel_source_files(kernel: str) -> list:
+    """The kernel's source file followed by every header of the package it
+    includes (#include "..."), transitively, in first-inclusion order: an
+    edit to any of them changes the compiled kernel."""
+    csrc = os.path.join(ROOT, "paper_2608_17379_amd", "csrc")
+    order, todo = [], [KERNEL_SOURCES[kernel]]
+    while todo:
+        name = todo.pop(0)
+        if name in order:
+            continue
+        order.append(name)
+        for line in open(os.path.join(csrc, name), encoding="utf-8"):
+            line = line.strip()
+            if line.startswith("#include \""):
+                inc = line.split('"')[1]
+                if os.path.exists(os.path.join(csrc, inc)):
+                    todo.append(inc)
+    return order
+
+
 def source_sha(kernel: str) -> str:
-    """Hash of the kernel's source with comments and blank lines removed, so
-    that a recorded traffic figure survives comment-only edits."""
-    path = os.path.join(ROOT, "paper_2608_17379_amd", "csrc", KERNEL_SOURCES[kernel])
+    """Hash of the kernel's source and its package headers with comments and
+    blank lines removed, so that a recorded traffic figure survives
+    comment-only edits but not a change of the compiled code."""
+    csrc = os.path.join(ROOT, "paper_2608_17379_amd", "csrc")
     code = []
-    for line in open(path, encoding="utf-8"):
-        line = line.split("//", 1)[0].rstrip()
-        if line:
-            code.append(line)
+    for name in kernel_source_files(kernel):
+        code.append(f"// file {name}")
+        for line in open(os.path.join(csrc, name), encoding="utf-8"):
+            line = line.split("//", 1)[0].rstrip()
+            if line:
+                code.append(line)
     return hashlib.sha256("\n".join(code).encode()).hexdigest()[:16]
 
 
@@ -112,6 +154,87 @@ def load_traffic(kernel: str, workload: str):
     if rec.get("source_sha") != source_sha(kernel):
         return None
     return rec.get("bytes_per_launch")
+
+
+def attention_bytes(kernel: str, w, x) -> float:
+    """Algorithmic HBM bytes of one launch: every input read once and every
+    output written once (bf16 rows of D values, fp32 per-row values).
+      fwd_kernel        reads Q, K, V; writes O, LSE
+      bwd_dq_kernel     reads Q, K, V, O, dO, LSE; writes dQ, Delta, LSE log2 e
+      dK/dV kernels     reads Q, K, V, dO, Delta, LSE log2 e; writes dK, dV"""
+    rows = x.q.shape[0] if w.varlen else w.B * w.S
+    nq, nkv = rows * w.Hq, rows * w.Hkv     # (row, head) pairs
+    row = w.D * 2
+    if kernel == "fwd_kernel":
+        return 2 * nq * row + 2 * nkv * row + 4 * nq
+    if kernel == "bwd_dq_kernel":
+        return 4 * nq * row + 2 * nkv * row + 3 * 4 * nq
+    return 2 * nq * row + 4 * nkv * row + 2 * 4 * nq
+
+
+def roofline(kernel: str, flop: float, nbytes: float, ms: float, workload: str,
+             hbm_work: bool = False) -> dict:
+    """Roofline object of one kernel.  The bound is the roof its algorithmic
+    work meets first: MFMA (flop / 2516.6 TFLOP/s) or HBM (bytes / 8 TB/s);
+    `hbm_work` reports an HBM-bound kernel's rate in GB/s of its algorithmic
+    bytes.  `traffic` is the measured HBM bytes per launch (None unless the
+    counters were taken on the current source), with the HBM rate they imply."""
+    hbm = hbm_work or nbytes / (PEAK_HBM_GBS * 1e9) > flop / (PEAK_BF16_TFLOPS * 1e12)
+    if hbm:
+        ach, peak, unit = nbytes / (ms * 1e-3) / 1e9, PEAK_HBM_GBS, "GB/s"
+    else:
+        ach, peak, unit = flop / (ms * 1e-3) / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
+    traffic = load_traffic(kernel, workload)
+    out = {"kernel": kernel, "bound": "hbm" if hbm else "mfma", "achieved": round(ach, 2),
+           "peak": peak, "unit": unit, "frac": round(ach / peak, 4), "traffic": traffic,
+           "algorithmic_bytes": round(nbytes)}
+    if flop:
+        out["arith_intensity"] = round(flop / nbytes, 1)
+    if traffic:
+        out["traffic_hbm_frac"] = round(traffic / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
+    return out
+
+
+def host_cpu() -> dict:
+    """Host threads the CPU leg may use (the process's CPU affinity, capped
+    by OMP_NUM_THREADS when that is set, as it is where the host is shared)
+    and the CPU model (/proc/cpuinfo, the source lscpu reads)."""
+    cpus = len(os.sched_getaffinity(0))
+    n = cpus
+    omp = os.environ.get("OMP_NUM_THREADS", "")
+    if omp.isdigit() and int(omp) > 0:
+        n = min(n, int(omp))
+    model = None
+    try:
+        for line in open("/proc/cpuinfo", encoding="utf-8"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"threads": n, "affinity_cpus": cpus, "model": model}
+
+
+class cpu_threads:
+    """Run the CPU leg on every usable host thread (host_cpu()), then
+    restore torch's thread count."""
+
+    def __enter__(self):
+        import torch
+        self.saved = torch.get_num_threads()
+        self.info = host_cpu()
+        torch.set_num_threads(self.info["threads"])
+        return self
+
+    def __exit__(self, *exc):
+        import torch
+        torch.set_num_threads(self.saved)
+        return False
+
+    def fields(self) -> dict:
+        import torch
+        return {"cores": torch.get_num_threads(), "cpu_model": self.info["model"],
+                "affinity_cpus": self.info["affinity_cpus"]}
 
 
 def cpu_baseline(w, x, seconds: float):
@@ -151,6 +274,7 @@ def cpu_baseline(w, x, seconds: float):
         "unit": "TFLOP/s",
         "cores": torch.get_num_threads(),
         "kind": "oracle",
+        "flop_convention": "fwd + bwd = 3.5 x the forward's causal-halved FLOP",
         "sample": f"{n_done} key/value-head slices ({G} query heads each; {len(slices)} per "
                   f"pass, {passes} pass(es)) of {w.name}, fp64 forward + backward, {dt:.1f} s",
     }
@@ -287,58 +411,112 @@ def cold_steps(step, steps: int, flush_bytes: int = 512 << 20):
 
 
 def time_steps(step, n_kernels: int, steps: int, warmup: int, warmup_seconds: float = 1.0):
-    """Warm up, then run two timed passes of `steps` steps: the first has no
-    events inside the steps (its time per step is the reported one), the
-    second records an event around every launch (per-kernel times).
-    `step(ev)` records ev[0] before its first launch and ev[1 + i] after
-    launch i.
+    """Warm up and time `steps` steps several ways.  `step(ev)` records ev[0]
+    before its first launch and ev[1 + i] after launch i.
 
-    Warm-up: `warmup` steps, then more back-to-back steps until
-    `warmup_seconds` have passed: the GPU's clock and power management take
-    about a second of sustained load to settle, and steps timed earlier run
-    up to 12 % slower.  If the host enqueues a step in less than half the
-    time the GPU takes to run it, the timed passes follow the warm-up
-    directly (the queue stays full); otherwise the GPU is first held by a
-    spin kernel while the host enqueues the pass, so that the timing is the
-    GPU's and not the host's launch rate.
-    Returns (ms per step, [ms per launch i], warm-up steps run)."""
+      * "early": `warmup` untimed steps (after a five-step probe), then
+        `steps` timed steps: the paper's protocol of a fixed warm-up count.
+      * "settled" (the reported value): more back-to-back steps until
+        `warmup_seconds` have passed since the probe, then `steps` timed
+        steps.  The GPU's clock and power management take about a second of
+        sustained load to settle; steps timed earlier run up to 12 % slower.
+      * "median": the median of `steps` per-step times, from an event
+        recorded between consecutive steps of a further pass (the paper
+        reports the median of its timed runs).
+      * per-kernel times: a last pass records an event around every launch.
+
+    Each timed pass has no events inside its steps (except the median and
+    per-kernel passes, as stated).  If the host enqueues a step in less than
+    half the time the GPU takes to run it, a pass's start event is recorded
+    right behind the steps before it, with the queue still full, so that it
+    starts on a busy GPU; otherwise the GPU is first held by a spin kernel
+    while the host enqueues the pass, so that the timing is the GPU's and
+    not the host's launch rate.
+    Returns a dict: ms_step (settled), early_ms, median_ms, kern (ms per
+    launch i), warmed (warm-up steps run before the settled pass),
+    early_warmup (before the early pass)."""
     import torch
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_kernels + 1)]
-           for _ in range(max(steps, 1))]
     # Host enqueue rate against GPU rate, on a few steps that cannot fill the
     # launch queue (once it is full, enqueueing waits for the GPU).
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
+    t_probe = time.perf_counter()
     probe = 5
     for _ in range(probe):
         step()
-    host_ms = (time.perf_counter() - t0) * 1e3 / probe
+    host_ms = (time.perf_counter() - t_probe) * 1e3 / probe
     torch.cuda.synchronize()
-    gpu_ms = (time.perf_counter() - t0) * 1e3 / probe
+    gpu_ms = (time.perf_counter() - t_probe) * 1e3 / probe
     hold = host_ms >= 0.5 * gpu_ms
+
+    def begin():
+        if hold:
+            torch.cuda.synchronize()
+            hold_gpu_for_enqueue(host_ms, steps)
+        ev = torch.cuda.Event(enable_timing=True)
+        ev.record()
+        return ev
+
+    def timed_pass():
+        start, end = begin(), torch.cuda.Event(enable_timing=True)
+        for _ in range(steps):
+            step()
+        end.record()
+        torch.cuda.synchronize()
+        return start.elapsed_time(end) / steps
+
     done = probe
-    t0 = time.perf_counter()
-    while done < warmup or time.perf_counter() - t0 < warmup_seconds:
+    for _ in range(warmup):
         step()
         done += 1
-    torch.cuda.synchronize()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    if hold:
-        hold_gpu_for_enqueue(host_ms, steps)
-    start.record()
-    for _ in range(steps):
+    early_warmup = done
+    early_ms = timed_pass()
+    done += steps
+    while done < warmup or time.perf_counter() - t_probe < warmup_seconds:
         step()
-    end.record()
+        done += 1
+    ms_step = timed_pass()
+
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    marks[0] = begin()
+    for i in range(steps):
+        step()
+        if i + 1 < steps:
+            marks[i + 1].record()
+    last = torch.cuda.Event(enable_timing=True)
+    last.record()
     torch.cuda.synchronize()
-    ms_step = start.elapsed_time(end) / steps
+    marks.append(last)
+    per_step = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(steps))
+    median_ms = per_step[steps // 2] if steps % 2 else \
+        0.5 * (per_step[steps // 2 - 1] + per_step[steps // 2])
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_kernels + 1)]
+           for _ in range(max(steps, 1))]
     if hold:
+        torch.cuda.synchronize()
         hold_gpu_for_enqueue(host_ms, steps)
     for i in range(steps):
         step(evs[i])
     torch.cuda.synchronize()
     kern = [sum(e[j].elapsed_time(e[j + 1]) for e in evs[:steps]) / steps
             for j in range(n_kernels)]
-    return ms_step, kern, done
+    return {"ms_step": ms_step, "early_ms": early_ms, "median_ms": median_ms, "kern": kern,
+            "warmed": done, "early_warmup": early_warmup}
+
+
+def timing_fields(t: dict, args, work: float, unit_scale: float) -> dict:
+    """The secondary timings of a bench line: `work` per step (FLOP or
+    bytes) over unit_scale gives the metric's unit per second."""
+    rate = lambda ms: round(work / (ms * 1e-3) / unit_scale, 2)
+    return {
+        "median": {"ms_per_step": round(t["median_ms"], 5), "value": rate(t["median_ms"]),
+                   "note": "median of the per-step times of a separate pass"},
+        "at_requested_warmup": {"warmup": t["early_warmup"],
+                                "ms_per_step": round(t["early_ms"], 5),
+                                "value": rate(t["early_ms"]),
+                                "note": "timed right after the requested warm-up count "
+                                        "(plus the five-step probe), before the clock settles"},
+    }
 
 
 # ---------------------------------------------------------------------------
@@ -368,6 +546,16 @@ def decode_bytes(x) -> dict:
     idx = 4 * (nnz + batch + 1)
     out = batch * w.Hq * (w.D * 2 + 4)
     return {"decode_split_kernel": kv + q + idx, "decode_merge_kernel": out}
+
+
+def prefill_bytes(x) -> float:
+    """Algorithmic HBM bytes of one paged prefill call: the queries, every
+    key and value row of every request once (per key/value head), the page
+    indices and index pointers, and the outputs (bf16 O, fp32 LSE)."""
+    w = x.workload
+    tq, nnz = x.q.shape[0], len(x.kv_indices)
+    return (2 * tq * w.Hq * w.D * 2 + 2 * nnz * w.Hkv * w.D * 2 + 4 * tq * w.Hq
+            + 4 * (nnz + 2 * (w.batch + 1)))
 
 
 def cpu_baseline_paged(x, seconds: float, unit_of):
@@ -432,9 +620,9 @@ def run_paged(args, w) -> int:
             if ev is not None:
                 ev[1 + i].record()
 
-    ms_step, kl, warmed = time_steps(step, len(kernels), args.steps, args.warmup,
-                                     args.warmup_seconds)
-    kern_ms = dict(zip(kernels, kl))
+    tm = time_steps(step, len(kernels), args.steps, args.warmup, args.warmup_seconds)
+    ms_step, warmed = tm["ms_step"], tm["warmed"]
+    kern_ms = dict(zip(kernels, tm["kern"]))
     gpu_state = sustained_state(step, args.state_seconds)
     if not (torch.isfinite(o.float()).all() and torch.isfinite(lse).all()):
         print("non-finite output", file=sys.stderr)
@@ -456,28 +644,27 @@ def run_paged(args, w) -> int:
         by = decode_bytes(x)
         total = sum(by.values())
         dom = max(kernels, key=lambda n: kern_ms[n])
-        ach = by[dom] / (kern_ms[dom] * 1e-3) / 1e9
         rec.update({"metric": f"paged decode HBM GB/s, {w.name}",
                     "value": round(total / (ms_step * 1e-3) / 1e9, 2), "unit": "GB/s",
                     "tflops": round(F / (ms_step * 1e-3) / 1e12, 4),
-                    "roofline": {"kernel": dom, "bound": "hbm", "achieved": round(ach, 2),
-                                 "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                                 "frac": round(ach / PEAK_HBM_GBS, 4),
-                                 "traffic": load_traffic(dom, w.name)}})
+                    "roofline": roofline(dom, 0.0, by[dom], kern_ms[dom], w.name,
+                                         hbm_work=True)})
+        rec.update(timing_fields(tm, args, total, 1e9))
         unit_of = lambda n, dt: (total * n / dt / 1e9, "GB/s")
     else:
         kn = kernels[0]
-        ach = F / (kern_ms[kn] * 1e-3) / 1e12
         rec.update({"metric": f"attention fwd TFLOP/s, {w.name}",
                     "value": round(F / (ms_step * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
                     "pct_peak": round(100 * F / (ms_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
-                    "roofline": {"kernel": kn, "bound": "mfma", "achieved": round(ach, 2),
-                                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                                 "frac": round(ach / PEAK_BF16_TFLOPS, 4),
-                                 "traffic": load_traffic(kn, w.name)}})
+                    "roofline": roofline(kn, F, prefill_bytes(x), kern_ms[kn], w.name)})
+        rec.update(timing_fields(tm, args, F, 1e12))
         unit_of = lambda n, dt: (F * n / dt / 1e12, "TFLOP/s")
-    rec["cpu_baseline"] = None if args.no_cpu_baseline else \
-        cpu_baseline_paged(x, args.cpu_seconds, unit_of)
+    if not args.no_cpu_baseline:
+        with cpu_threads() as ct:
+            rec["cpu_baseline"] = cpu_baseline_paged(x, args.cpu_seconds, unit_of)
+            rec["cpu_baseline"].update(ct.fields())
+    else:
+        rec["cpu_baseline"] = None
     print(json.dumps(rec), flush=True)
     return 0
 
@@ -510,14 +697,13 @@ def run_gemm(args, w) -> int:
             ev[1].record()
 
     attn.attn_gemm_bf16_nt(a, b, c)   # shape and pointer checks once, through the binding
-    ms_step, (kern_ms,), warmed = time_steps(step, 1, args.steps, args.warmup,
-                                             args.warmup_seconds)
+    tm = time_steps(step, 1, args.steps, args.warmup, args.warmup_seconds)
+    ms_step, (kern_ms,), warmed = tm["ms_step"], tm["kern"], tm["warmed"]
     gpu_state = sustained_state(step, args.state_seconds)
     if not torch.isfinite(c.float()).all():
         print("non-finite output", file=sys.stderr)
         return 1
     F = 2.0 * w.M * w.N * w.K
-    ach = F / (kern_ms * 1e-3) / 1e12
     rec = {"metric": f"bf16 GEMM TFLOP/s, {w.name}",
            "value": round(F / (ms_step * 1e-3) / 1e12, 2), "unit": "TFLOP/s", "n_gpus": 1,
            "steps": args.steps, "warmup": warmed, "warmup_requested": args.warmup,
@@ -528,23 +714,23 @@ def run_gemm(args, w) -> int:
            "gpu_state": gpu_state,
            "pct_peak": round(100 * F / (ms_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
            "kernel_ms": {"gemm_nt_kernel": round(kern_ms, 5)},
-           "roofline": {"kernel": "gemm_nt_kernel", "bound": "mfma", "achieved": round(ach, 2),
-                        "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                        "frac": round(ach / PEAK_BF16_TFLOPS, 4),
-                        "traffic": load_traffic("gemm_nt_kernel", w.name)},
+           "roofline": roofline("gemm_nt_kernel", F, 2.0 * (w.M * w.K + w.N * w.K + w.M * w.N),
+                                kern_ms, w.name),
            "cpu_baseline": None}
+    rec.update(timing_fields(tm, args, F, 1e12))
     if not args.no_cpu_baseline:
         # The oracle on whole rows of C (64 rows at a time) until the budget is spent.
-        t0, rows = time.perf_counter(), 0
-        while rows == 0 or time.perf_counter() - t0 < args.cpu_seconds:
-            r0 = rows % w.M
-            oracle.gemm_nt(a_h[r0:r0 + 64], b_h)
-            rows += 64
-        dt = time.perf_counter() - t0
-        rec["cpu_baseline"] = {"value": round(2.0 * rows * w.N * w.K / dt / 1e12, 6),
-                               "unit": "TFLOP/s", "cores": torch.get_num_threads(),
-                               "kind": "oracle",
-                               "sample": f"{rows} rows of C ({rows}x{w.N}x{w.K}), fp64, {dt:.1f} s"}
+        with cpu_threads() as ct:
+            t0, rows = time.perf_counter(), 0
+            while rows == 0 or time.perf_counter() - t0 < args.cpu_seconds:
+                r0 = rows % w.M
+                oracle.gemm_nt(a_h[r0:r0 + 64], b_h)
+                rows += 64
+            dt = time.perf_counter() - t0
+            rec["cpu_baseline"] = {"value": round(2.0 * rows * w.N * w.K / dt / 1e12, 6),
+                                   "unit": "TFLOP/s", "kind": "oracle",
+                                   "sample": f"{rows} rows of C ({rows}x{w.N}x{w.K}), fp64, "
+                                             f"{dt:.1f} s", **ct.fields()}
     print(json.dumps(rec), flush=True)
     return 0
 
@@ -643,9 +829,9 @@ def main(argv=None) -> int:
                                    q.shape[0] if w.varlen else 0, w.D, w.causal, w.varlen)
     dkdv = "bwd_dkdv4_kernel" if form == attn.ATTN_BWD_DKDV_TWO_PER_CU else "bwd_dkdv_kernel"
     kernels = ("fwd_kernel", "bwd_dq_kernel", dkdv)
-    ms_step, kl, warmed = time_steps(step, len(kernels), args.steps, args.warmup,
-                                     args.warmup_seconds)
-    kern_ms = dict(zip(kernels, kl))
+    tm = time_steps(step, len(kernels), args.steps, args.warmup, args.warmup_seconds)
+    ms_step, warmed = tm["ms_step"], tm["warmed"]
+    kern_ms = dict(zip(kernels, tm["kern"]))
     ms_cold = cold_steps(step, args.cold_steps) if args.cold_steps > 0 else None
     gpu_state = sustained_state(step, args.state_seconds)
     for t in (o, lse, dq, dk, dv):
@@ -657,7 +843,7 @@ def main(argv=None) -> int:
     total = 3.5 * F
     value = total / (ms_step * 1e-3) / 1e12
     dom = max(kernels, key=lambda n: kern_ms[n])
-    achieved = GEMMS[dom] / 2 * F / (kern_ms[dom] * 1e-3) / 1e12
+    kflop = {n: GEMMS[n] / 2 * F for n in kernels}
     fwd_ms = kern_ms["fwd_kernel"]
     bwd_ms = kern_ms["bwd_dq_kernel"] + kern_ms[dkdv]
     cfg = {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "S": w.S, "D": w.D,
@@ -685,15 +871,11 @@ def main(argv=None) -> int:
         "fwd_pct_peak": round(100 * F / (fwd_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
         "bwd_pct_peak": round(100 * 2.5 * F / (bwd_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
         "kernel_ms": {n: round(t, 4) for n, t in kern_ms.items()},
-        "roofline": {
-            "kernel": dom,
-            "bound": "mfma",
-            "achieved": round(achieved, 2),
-            "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": load_traffic(dom, w.name),
-        },
+        "kernel_tflops": {n: {"algorithmic": round(kflop[n] / (kern_ms[n] * 1e-3) / 1e12, 2),
+                              "executed": round(GEMMS_EXECUTED[n] / 2 * F
+                                                / (kern_ms[n] * 1e-3) / 1e12, 2)}
+                          for n in kernels},
+        "roofline": roofline(dom, kflop[dom], attention_bytes(dom, w, x), kern_ms[dom], w.name),
         "cpu_baseline": None,
         "cold": None if ms_cold is None else {
             "ms_per_step": round(ms_cold, 4),
@@ -702,8 +884,11 @@ def main(argv=None) -> int:
             "note": "median step after a 512 MiB write flushes L2 and MALL (write not timed)"},
         "gpu_state": gpu_state,
     }
+    rec.update(timing_fields(tm, args, total, 1e12))
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(w, x, args.cpu_seconds)
+        with cpu_threads() as ct:
+            rec["cpu_baseline"] = cpu_baseline(w, x, args.cpu_seconds)
+            rec["cpu_baseline"].update(ct.fields())
     print(json.dumps(rec), flush=True)
     return 0
 

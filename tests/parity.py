@@ -7,6 +7,7 @@ Tolerances (bf16 inputs, fp32 accumulation, bf16 outputs):
            score products are exact in fp32 and only the fp32 summation and
            the ~1-ulp hardware exp2/log2 contribute)
 """
+import math
 import sys
 
 import torch
@@ -78,6 +79,59 @@ def check_all(got, ref, label: str):
     for n in ("dq_rel", "dk_rel", "dv_rel"):
         assert errs[n] <= GRAD_RELL2, (label, n, errs)
     return errs
+
+
+class WholeTensorParity:
+    """Error metrics of whole output tensors, accumulated over the
+    independent slices they are compared in (one segment and one key/value
+    head with its whole query-head group per slice; together the slices
+    cover every element exactly once).
+
+    Each slice must meet the gates on its own; at the end the whole tensors
+    must too: O and LSE max-abs over every element, dQ/dK/dV relative L2 with
+    the sums of squares taken over every element.  The paper's checker,
+    allclose(atol=rtol=1e-2), is reported as the fraction of elements of each
+    output that fail it (informational)."""
+
+    NAMES = ("o", "lse", "dq", "dk", "dv")
+
+    def __init__(self, label: str):
+        self.label = label
+        self.maxabs = {"o": 0.0, "lse": 0.0}
+        self.sq_err = {n: 0.0 for n in ("dq", "dk", "dv")}
+        self.sq_ref = {n: 0.0 for n in ("dq", "dk", "dv")}
+        self.close_fail = {n: 0 for n in self.NAMES}
+        self.elems = {n: 0 for n in self.NAMES}
+        self.slices = 0
+
+    def add(self, got, ref, slice_label: str):
+        check_all(got, ref, f"{self.label} {slice_label}")
+        for n, x, r in zip(self.NAMES, got, ref):
+            x64, r64 = x.detach().double().cpu(), r.detach().double().cpu()
+            if n in self.maxabs:
+                self.maxabs[n] = max(self.maxabs[n], max_abs(x64, r64))
+            else:
+                self.sq_err[n] += float(((x64 - r64) ** 2).sum())
+                self.sq_ref[n] += float((r64 ** 2).sum())
+            fin = torch.isfinite(r64)
+            bad = ~torch.isclose(x64, r64, rtol=1e-2, atol=1e-2) & fin
+            self.close_fail[n] += int(bad.sum())
+            self.elems[n] += x64.numel()
+        self.slices += 1
+
+    def finish(self):
+        rel = {n: math.sqrt(self.sq_err[n]) / (math.sqrt(self.sq_ref[n]) or 1.0)
+               for n in self.sq_err}
+        frac = {n: self.close_fail[n] / max(1, self.elems[n]) for n in self.NAMES}
+        announce(f"{self.label} whole tensors over {self.slices} slices: "
+                 f"o_maxabs={self.maxabs['o']:.3g} lse_maxabs={self.maxabs['lse']:.3g} "
+                 + " ".join(f"{n}_rel={rel[n]:.3g}" for n in rel) + " allclose(1e-2) failing "
+                 + " ".join(f"{n}={frac[n]:.2e}" for n in self.NAMES))
+        assert self.maxabs["o"] <= O_MAXABS, (self.label, self.maxabs)
+        assert self.maxabs["lse"] <= LSE_MAXABS, (self.label, self.maxabs)
+        for n, e in rel.items():
+            assert e <= GRAD_RELL2, (self.label, n, rel)
+        return self.maxabs, rel, frac
 
 
 def oracle_all(x: wl.Inputs, causal: bool, scale: float):

@@ -17,9 +17,10 @@ allclose(atol=rtol=1e-2), is reported as well.
 
 Small shapes cover every tail (M, N not multiples of the 256 x 256 tile; K
 not a multiple of the 64-wide K step); the paper's 8192 x 7168 x 5120
-workload is compared on sampled rows (every column), which the oracle
-computes exactly.
+workload is compared over its whole output.
 """
+import math
+
 import pytest
 import torch
 
@@ -95,6 +96,10 @@ def test_gemm_deterministic():
 
 @pytest.mark.parametrize("name", list(wl.GEMM_WORKLOADS))
 def test_full_gemm_workload(name):
+    """The paper's GEMM at full size: every element of C against the oracle
+    and its per-element bound (the rows are compared in blocks only to bound
+    the fp64 temporaries; the relative L2 error is taken over the whole
+    output)."""
     w = wl.GEMM_WORKLOADS[name]
     a, b = wl.make_gemm_inputs(w, 0)
     announce(f"full-size {name}")
@@ -102,6 +107,21 @@ def test_full_gemm_workload(name):
     torch.cuda.synchronize()
     c = c.cpu()
     assert torch.isfinite(c.float()).all()
-    # rows in the first, middle and last row tiles, at tile edges and inside
-    rows = sorted({0, 1, 31, 32, 127, 255, 256, 257, 1000, 4095, 4096, 6001, 8190, 8191})
-    _check(c[rows], a[rows], b, f"{name} rows {rows}")
+    K = w.K
+    gamma = K * 2.0 ** -23 / (1 - K * 2.0 ** -23)
+    sq_err = sq_ref = 0.0
+    worst, close_fail = 0.0, 0
+    for r0 in range(0, w.M, 1024):
+        r1 = min(w.M, r0 + 1024)
+        r = oracle.gemm_nt(a[r0:r1], b)
+        bound = 2.0 ** -8 * r.abs() + (1 + 2.0 ** -8) * gamma * oracle.abs_products(a[r0:r1], b)
+        err = (c[r0:r1].double() - r).abs()
+        assert (err <= bound).all(), (name, r0)
+        worst = max(worst, float((err / bound.clamp_min(1e-300)).max()))
+        sq_err += float((err ** 2).sum())
+        sq_ref += float((r ** 2).sum())
+        close_fail += int((err > 1e-2 + 1e-2 * r.abs()).sum())
+    rel = math.sqrt(sq_err / sq_ref)
+    announce(f"{name} whole output: max err/bound={worst:.3g} rel_l2={rel:.3g} "
+             f"allclose(1e-2) failing {close_fail / (w.M * w.N):.2e}")
+    assert rel <= 5e-3, (name, rel)

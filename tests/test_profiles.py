@@ -49,3 +49,20 @@ def test_record_is_consistent(key):
 def test_headline_kernels_have_records():
     for kernel in ("fwd_kernel", "bwd_dq_kernel", "bwd_dkdv4_kernel"):
         assert f"{kernel}:{wl.HEADLINE}" in DB
+
+
+@pytest.mark.parametrize("kernel", sorted(bench.KERNEL_SOURCES))
+def test_hashed_sources_follow_includes(kernel):
+    """The source hash that ties a record to the code covers the kernel's
+    file and every package header it includes, directly or not."""
+    files = bench.kernel_source_files(kernel)
+    csrc = os.path.join(ROOT, "paper_2608_17379_amd", "csrc")
+    assert files[0] == bench.KERNEL_SOURCES[kernel]
+    for name in files:
+        for line in open(os.path.join(csrc, name), encoding="utf-8"):
+            line = line.strip()
+            if line.startswith('#include "'):
+                inc = line.split('"')[1]
+                if os.path.exists(os.path.join(csrc, inc)):
+                    assert inc in files, (kernel, name, inc)
+    assert "device_common.hpp" in files and "attn_kernels.hpp" in files

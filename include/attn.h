@@ -67,9 +67,11 @@ typedef enum {
   ATTN_ERR_ALIGN = -5,      /* a pointer is not 16-byte aligned */
   ATTN_ERR_WORKSPACE = -6,  /* workspace null or smaller than required */
   ATTN_ERR_HIP = -7,        /* a kernel launch failed (hipGetLastError) */
-  ATTN_ERR_VALUE = -8       /* scale not finite or not > 0, causal not 0/1,
+  ATTN_ERR_VALUE = -8,      /* scale not finite or not > 0, causal not 0/1,
                                max_seqlen (max_qlen, max_kvlen) < 1, or a bad
                                backward phase mask */
+  ATTN_ERR_SCRATCH = -9     /* attn_bwd_noalloc: the problem needs more than
+                               ATTN_BWD_NOALLOC_SCRATCH_BYTES of scratch */
 } attn_status_t;
 
 /*
@@ -97,6 +99,28 @@ int attn_bwd(const void* q, const void* k, const void* v, const void* o,
              const float* lse, const void* dO, void* dq, void* dk, void* dv,
              int B, int Hq, int Hkv, int S, int D, int causal, float scale,
              void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Backward, fixed length, for callers that cannot allocate memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): attn_bwd without a workspace argument.  Its scratch (the
+ * same fp32 Delta and L log2(e) arrays) is a device array inside the
+ * library of ATTN_BWD_NOALLOC_SCRATCH_BYTES, which every GPU the library
+ * runs on holds until the process ends; the call itself allocates nothing.
+ * A problem whose attn_bwd_workspace_size exceeds it (B * Hq * S above
+ * 2,097,152) returns ATTN_ERR_SCRATCH before any GPU work.  Every call on
+ * one GPU uses that GPU's one scratch array: calls that can overlap on a
+ * GPU (other streams, other host threads) race and must be ordered by the
+ * caller.  The first call on a device looks up the array's address there
+ * (hipGetSymbolAddress, with that device made current for the lookup).
+ * Arguments, layouts, results and errors otherwise as for attn_bwd; the
+ * results are bitwise equal to attn_bwd's.
+ */
+#define ATTN_BWD_NOALLOC_SCRATCH_BYTES (16u << 20)
+int attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o,
+                     const float* lse, const void* dO, void* dq, void* dk, void* dv,
+                     int B, int Hq, int Hkv, int S, int D, int causal, float scale,
+                     hipStream_t stream);
 
 /*
  * Forward, packed variable length (ragged prefill).  total = T rows;

@@ -21,10 +21,11 @@ ATTN_OK = 0
 STATUS_NAMES = {
     0: "ATTN_OK", -1: "ATTN_ERR_NULL", -2: "ATTN_ERR_SHAPE", -3: "ATTN_ERR_GQA",
     -4: "ATTN_ERR_HEAD_DIM", -5: "ATTN_ERR_ALIGN", -6: "ATTN_ERR_WORKSPACE",
-    -7: "ATTN_ERR_HIP", -8: "ATTN_ERR_VALUE",
+    -7: "ATTN_ERR_HIP", -8: "ATTN_ERR_VALUE", -9: "ATTN_ERR_SCRATCH",
 }
 EXPORTS = ("attn_fwd", "attn_bwd", "attn_bwd_workspace_size", "attn_fwd_varlen",
            "attn_bwd_varlen", "attn_bwd_varlen_workspace_size", "attn_bwd_phases",
+           "attn_bwd_noalloc",
            "attn_bwd_varlen_phases", "attn_bwd_dkdv_form", "attn_fwd_paged_workspace_size",
            "attn_fwd_paged",
            "attn_decode_paged_workspace_size",
@@ -36,6 +37,7 @@ ATTN_BWD_DKDV_ONE_PER_CU = 4
 ATTN_BWD_DKDV_TWO_PER_CU = 8
 ATTN_DECODE_SPLIT = 1
 ATTN_DECODE_MERGE = 2
+ATTN_BWD_NOALLOC_SCRATCH_BYTES = 16 << 20
 
 
 class AttnError(RuntimeError):
@@ -67,6 +69,8 @@ def lib() -> ctypes.CDLL:
         l.attn_bwd_varlen_workspace_size.restype = _Z
         l.attn_bwd_varlen.argtypes = [_P] * 10 + [_I] * 7 + [_F, _P, _Z, _P]
         l.attn_bwd_varlen.restype = _I
+        l.attn_bwd_noalloc.argtypes = [_P] * 9 + [_I] * 6 + [_F, _P]
+        l.attn_bwd_noalloc.restype = _I
         l.attn_bwd_phases.argtypes = [_P] * 9 + [_I] * 6 + [_F, _P, _Z, _I, _P]
         l.attn_bwd_phases.restype = _I
         l.attn_bwd_varlen_phases.argtypes = [_P] * 10 + [_I] * 7 + [_F, _P, _Z, _I, _P]
@@ -177,6 +181,24 @@ def attn_bwd(q, k, v, o, lse, dO, dq, dk, dv, causal: bool, scale: float,
                         float(scale), _ptr(workspace, "workspace", torch.uint8),
                         workspace.numel(), _stream(stream))
     _check(st, "attn_bwd")
+
+
+def attn_bwd_noalloc(q, k, v, o, lse, dO, dq, dk, dv, causal: bool, scale: float,
+                     stream=None) -> None:
+    """attn_bwd with the library's own device scratch instead of a
+    workspace (for callers that cannot allocate); calls that can overlap on
+    one GPU race."""
+    B, Hq, S, D = q.shape
+    Hkv = k.shape[1]
+    for t, n, hh in ((k, "k", Hkv), (v, "v", Hkv), (o, "o", Hq), (dO, "dO", Hq),
+                     (dq, "dq", Hq), (dk, "dk", Hkv), (dv, "dv", Hkv)):
+        _shape(t, (B, hh, S, D), n)
+    _shape(lse, (B, Hq, S), "lse")
+    st = lib().attn_bwd_noalloc(_ptr(q, "q"), _ptr(k, "k"), _ptr(v, "v"), _ptr(o, "o"),
+                                _ptr(lse, "lse", torch.float32), _ptr(dO, "dO"), _ptr(dq, "dq"),
+                                _ptr(dk, "dk"), _ptr(dv, "dv"), B, Hq, Hkv, S, D,
+                                int(bool(causal)), float(scale), _stream(stream))
+    _check(st, "attn_bwd_noalloc")
 
 
 def attn_bwd_dkdv_form(nseg: int, Hkv: int, S: int, total: int, D: int, causal: bool,

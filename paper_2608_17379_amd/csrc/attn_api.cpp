@@ -3,7 +3,9 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <initializer_list>
+#include <mutex>
 
 #include "../../include/attn.h"
 #include "attn_kernels.hpp"
@@ -195,6 +197,47 @@ size_t delta_bytes(int64_t rows_times_heads) {
   return 2 * (size_t)((rows_times_heads * 4 + 255) / 256 * 256);
 }
 
+// ---------------------------------------------------------------------------
+// Scratch of attn_bwd_noalloc: the backward's Delta and L log2(e) arrays in a
+// file-scope device array instead of a caller workspace.  Each GPU the
+// library runs on holds its own copy until the process ends.  Host code
+// never passes the array's name to a kernel (on the host it only stands for
+// the device symbol): the device address comes from hipGetSymbolAddress,
+// taken once per device with that device current, and is kept per device.
+// ---------------------------------------------------------------------------
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[ATTN_BWD_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+// Device address of `scratch` on the device `stream` belongs to.
+int scratch_for(hipStream_t stream, void** out) {
+  hipDevice_t dev = 0;
+  if (hipStreamGetDevice(stream, &dev) != hipSuccess) return ATTN_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return ATTN_ERR_HIP;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      int cur = 0;
+      if (hipGetDevice(&cur) != hipSuccess) return ATTN_ERR_HIP;
+      if (cur != dev && hipSetDevice(dev) != hipSuccess) return ATTN_ERR_HIP;
+      const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (cur != dev && hipSetDevice(cur) != hipSuccess) return ATTN_ERR_HIP;
+      if (e != hipSuccess || !p) return ATTN_ERR_HIP;
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return ATTN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -246,6 +289,29 @@ int attn_bwd(const void* q, const void* k, const void* v, const void* o, const f
              hipStream_t stream) {
   return attn_bwd_phases(q, k, v, o, lse, dO, dq, dk, dv, B, Hq, Hkv, S, D, causal, scale,
                          workspace, workspace_bytes, ATTN_BWD_DQ | ATTN_BWD_DKDV, stream);
+}
+
+int attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o,
+                     const float* lse, const void* dO, void* dq, void* dk, void* dv, int B,
+                     int Hq, int Hkv, int S, int D, int causal, float scale,
+                     hipStream_t stream) {
+  int st = check_common(Hq, Hkv, D, causal, scale);
+  if (st != ATTN_OK) return st;
+  if (B < 0 || check_rows(S) != ATTN_OK) return ATTN_ERR_SHAPE;
+  if ((int64_t)B * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
+  if (B == 0 || S == 0) return ATTN_OK;
+  const size_t need = attn_bwd_workspace_size(B, Hq, Hkv, S, D);
+  if (need > ATTN_BWD_NOALLOC_SCRATCH_BYTES) return ATTN_ERR_SCRATCH;
+  if (any_null({q, k, v, o, lse, dO, dq, dk, dv})) return ATTN_ERR_NULL;
+  if (any_misaligned({q, k, v, o, lse, dO, dq, dk, dv})) return ATTN_ERR_ALIGN;
+  void* ws = nullptr;
+  if ((st = scratch_for(stream, &ws)) != ATTN_OK) return st;
+  // The dQ kernel writes Delta and L log2(e) of every row before the dK/dV
+  // kernel reads them (rows past a segment end are never read), so the
+  // scratch needs no clearing between calls.
+  return bwd_common(q, k, v, o, lse, dO, dq, dk, dv, fixed_layout(B, Hq, Hkv, S, D), D, causal,
+                    scale, ws, ATTN_BWD_NOALLOC_SCRATCH_BYTES, need,
+                    ATTN_BWD_DQ | ATTN_BWD_DKDV, stream);
 }
 
 int attn_fwd_varlen(const void* q, const void* k, const void* v, void* o, float* lse,
@@ -454,6 +520,9 @@ const char* attn_status_string(int status) {
     case ATTN_ERR_VALUE:
       return "scale is not finite and > 0, causal is not 0 or 1, max_seqlen < 1, or a bad phase "
              "mask";
+    case ATTN_ERR_SCRATCH:
+      return "the backward needs more scratch than attn_bwd_noalloc holds "
+             "(ATTN_BWD_NOALLOC_SCRATCH_BYTES)";
     default: return "unknown status";
   }
 }

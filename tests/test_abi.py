@@ -128,7 +128,7 @@ def test_workspace_validation():
 
 
 def test_status_strings():
-    for code in range(-8, 1):
+    for code in range(-9, 1):
         s = attn.attn_status_string(code)
         assert s and s != "unknown status"
     assert attn.attn_status_string(-99) == "unknown status"
@@ -273,3 +273,33 @@ def test_dkdv_form_rule():
     assert l.attn_bwd_dkdv_form(1, 1, 128, 0, 128, 2, 0) == -8
     with pytest.raises(attn.AttnError):
         form(1, 1, 128, 0, 80, True, False)
+
+
+def test_noalloc_validation_before_any_gpu_call():
+    """attn_bwd_noalloc checks its sizes, its scratch limit and its pointers
+    on the host and returns before any GPU call."""
+    l = attn.lib()
+
+    def call(**kw):
+        a = dict(p=A, B=1, Hq=2, Hkv=2, S=64, D=64, causal=1, scale=0.125)
+        a.update(kw)
+        ptrs = [a.get(n, a["p"]) for n in ("q", "k", "v", "o", "lse", "dO", "dq", "dk", "dv")]
+        return l.attn_bwd_noalloc(*ptrs, a["B"], a["Hq"], a["Hkv"], a["S"], a["D"], a["causal"],
+                                  a["scale"], None)
+
+    limit = attn.ATTN_BWD_NOALLOC_SCRATCH_BYTES
+    assert limit == 16 << 20
+    # B * Hq * S = 2^21 rows x heads fit exactly (two 4-byte arrays); one more
+    # 64-row block does not.
+    assert attn.attn_bwd_workspace_size(1, 32, 32, 65536, 128) == limit
+    assert call(B=1, Hq=32, Hkv=32, S=65536 + 64, D=128, p=0) == -9
+    assert call(B=2, Hq=32, Hkv=32, S=65536, D=128) == -9
+    assert call(B=1, Hq=32, Hkv=32, S=65536, D=128, p=0) == -1   # fits: pointers checked next
+    assert call(q=0) == -1
+    assert call(dv=A + 8) == -5
+    assert call(D=80) == -4
+    assert call(Hq=3, Hkv=2) == -3
+    assert call(scale=0.0) == -8
+    assert call(B=-1) == -2
+    assert call(B=0, p=0) == 0   # no rows: a no-op
+    assert "noalloc" in attn.attn_status_string(-9)

@@ -121,6 +121,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
       for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
     float mref = -INFINITY;   // reference max of scale*log2(e)*s for query qrow
     float lsum = 0.f;         // this lane's share of the row sum, relative to mref
+    // ... and of the sum of P rounded to bf16, the weights the PV products
+    // actually use.  O is normalised by this sum, so that its weights add up
+    // to one and the rounding of P largely cancels; L keeps the fp32 sum.
+    float lq = 0.f;
+    const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3f803f80u);
     const float sl2 = a.scale_log2;
     // Fields used inside the lambdas below, as plain values (capturing the
     // kernel argument itself can make the compiler spill it to scratch).
@@ -199,6 +204,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
         // (both maxima -inf), whose O and l are still 0.
         const float alpha = mnew == -INFINITY ? 1.f : fast_exp2(mref - mnew);
         lsum *= alpha;
+        lq *= alpha;
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
 #pragma unroll
@@ -219,9 +225,22 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
 
       // O^T[d][q] += sum_key V^T[d][key] P^T[key][q]; chunk c = keys 16c..16c+15,
       // V^T read transposed out of the row-major V tile.
+      float lq1 = 0.f;
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        const u32x4 pb = pack_chunk(s[c >> 1], c & 1);
+        // P^T chunk c as bf16 pairs; each pair is also summed as rounded
+        // (v_dot2 with (1, 1)) as soon as it is packed.
+        u32x4 pb;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t w = pack_bf16(s[c >> 1][8 * (c & 1) + 2 * j],
+                                       s[c >> 1][8 * (c & 1) + 2 * j + 1]);
+          pb[j] = w;
+          if (j & 1)
+            lq1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, lq1, false);
+          else
+            lq = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, lq, false);
+        }
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
           const u32x2 lo = ld_tr(vt_lds + vr.tr[db][0] + 16 * c * P);
@@ -229,6 +248,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
           oacc[db] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb, oacc[db]);
         }
       }
+      lq += lq1;
     };
     // One tile: wait for its loads (this wavefront's, then everyone's through
     // the barrier, which also frees the stage read one tile earlier), start the
@@ -270,9 +290,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
     // Epilogue: O = O / l, L = (m + log2 l) ln 2; or, for one chunk of
     // several, the chunk's O / l and m + log2 l (base 2) as a partial result.
     lsum += swap_halves(lsum);
+    lq += swap_halves(lq);
     if (nch > 1) {
       if (qrow < seg.len) {
-        const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+        const float inv = lq > 0.f ? 1.f / lq : 0.f;
         const int64_t slot = ((int64_t)(seg.start + qrow) * L.Hq + h) * a.nsplit + chunk;
         float* po = a.part_o + slot * D + 4 * half;
 #pragma unroll
@@ -286,7 +307,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
         if (half == 0) a.part_lse[slot] = lsum > 0.f ? mref + log2f(lsum) : -INFINITY;
       }
     } else if (qrow < seg.len) {
-      const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+      const float inv = lq > 0.f ? 1.f / lq : 0.f;
       uint16_t* op = a.o + qoff + (int64_t)qrow * L.q_row;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)

@@ -78,6 +78,15 @@ Layout packed_layout(const int* cu, int nseq, int max_seqlen, int total, int Hq,
   return L;
 }
 
+// The forward and the dQ kernel run one 1-D grid over (query block, query
+// head) in the XCD-aware order; it must fit a launch.
+bool grid_too_large(int64_t nseg, int Hq, int Hkv, int64_t rows) {
+  const int64_t nkv = nseg * Hkv;
+  const int64_t n = (int64_t)attn::kXcds * ((nkv + attn::kXcds - 1) / attn::kXcds) * (Hq / Hkv) *
+                    ((rows + 127) / 128);
+  return n > 0x7fffffff;
+}
+
 bool any_null(std::initializer_list<const void*> ps) {
   for (const void* p : ps)
     if (!p) return true;
@@ -248,6 +257,7 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
   if (st != ATTN_OK) return st;
   if (B < 0 || (st = check_rows(S)) != ATTN_OK) return ATTN_ERR_SHAPE;
   if ((int64_t)B * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
+  if (grid_too_large(B, Hq, Hkv, S)) return ATTN_ERR_SHAPE;
   if (B == 0 || S == 0) return ATTN_OK;
   return fwd_common(q, k, v, o, lse, fixed_layout(B, Hq, Hkv, S, D), D, causal, scale, stream);
 }
@@ -276,6 +286,7 @@ int attn_bwd_phases(const void* q, const void* k, const void* v, const void* o, 
   if (st != ATTN_OK) return st;
   if (B < 0 || check_rows(S) != ATTN_OK) return ATTN_ERR_SHAPE;
   if ((int64_t)B * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
+  if (grid_too_large(B, Hq, Hkv, S)) return ATTN_ERR_SHAPE;
   if (!valid_bwd_phases(phases)) return ATTN_ERR_VALUE;
   if (B == 0 || S == 0) return ATTN_OK;
   return bwd_common(q, k, v, o, lse, dO, dq, dk, dv, fixed_layout(B, Hq, Hkv, S, D), D, causal,
@@ -299,6 +310,7 @@ int attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o,
   if (st != ATTN_OK) return st;
   if (B < 0 || check_rows(S) != ATTN_OK) return ATTN_ERR_SHAPE;
   if ((int64_t)B * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
+  if (grid_too_large(B, Hq, Hkv, S)) return ATTN_ERR_SHAPE;
   if (B == 0 || S == 0) return ATTN_OK;
   const size_t need = attn_bwd_workspace_size(B, Hq, Hkv, S, D);
   if (need > ATTN_BWD_NOALLOC_SCRATCH_BYTES) return ATTN_ERR_SCRATCH;
@@ -321,6 +333,7 @@ int attn_fwd_varlen(const void* q, const void* k, const void* v, void* o, float*
   if (st != ATTN_OK) return st;
   if (nseq < 0 || total < 0 || check_rows(max_seqlen) != ATTN_OK) return ATTN_ERR_SHAPE;
   if ((int64_t)nseq * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
+  if (grid_too_large(nseq, Hq, Hkv, max_seqlen)) return ATTN_ERR_SHAPE;
   if (nseq == 0 || total == 0) return ATTN_OK;
   if (max_seqlen < 1) return ATTN_ERR_VALUE;
   if (!cu_seqlens) return ATTN_ERR_NULL;
@@ -345,6 +358,7 @@ int attn_bwd_varlen_phases(const void* q, const void* k, const void* v, const vo
   if (st != ATTN_OK) return st;
   if (nseq < 0 || total < 0 || check_rows(max_seqlen) != ATTN_OK) return ATTN_ERR_SHAPE;
   if ((int64_t)nseq * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
+  if (grid_too_large(nseq, Hq, Hkv, max_seqlen)) return ATTN_ERR_SHAPE;
   if (!valid_bwd_phases(phases)) return ATTN_ERR_VALUE;
   if (nseq == 0 || total == 0) return ATTN_OK;
   if (max_seqlen < 1) return ATTN_ERR_VALUE;

@@ -84,11 +84,13 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
   const int l32 = lane & 31, half = lane >> 5;
 
   const Layout L = a.L;
-  const int z = blockIdx.x / L.Hq, h = blockIdx.x % L.Hq;
+  int gk, j, p;
+  if (!xcd_decode((int)blockIdx.x, a.xo, gk, j, p)) return;
+  const int z = gk / L.Hkv;
+  const int h = (gk % L.Hkv) * L.group + j;
   const int hk = h / L.group;
   const Segment seg = segment_of(L, z);
   const int nqt = (seg.len + kQM - 1) / kQM;
-  const int p = (int)blockIdx.y;
   if (p >= nqt) return;
 
   // Fields used inside the lambdas below, as plain values (capturing the
@@ -379,7 +381,7 @@ __global__ __launch_bounds__(64 * kDkvWaves, 1) void bwd_dkdv_kernel(BwdArgs a) 
 
   auto issue = [&](int n, int st) __attribute__((always_inline)) {
     const int g = n / per_head;
-    const int qb = (it0 + n % per_head) * kTileRows;
+    const int qb = (it0 + per_head - 1 - n % per_head) * kTileRows;
     const int h = hk * group + g;
     const int64_t qoff = qseg + (int64_t)h * q_head;
     dma_tile<D>(qdma, rows_desc(qbase + qoff, qb, len, q_row_b), sbase + SM::Q + st * SM::TILE,
@@ -413,7 +415,7 @@ __global__ __launch_bounds__(64 * kDkvWaves, 1) void bwd_dkdv_kernel(BwdArgs a) 
     const uint16_t* dout = reinterpret_cast<const uint16_t*>(smem + SM::DO + st * SM::TILE);
     const float* lse = reinterpret_cast<const float*>(smem + SM::LSE + st * 256);
     const float* del = reinterpret_cast<const float*>(smem + SM::DEL + st * 256);
-    const int qs0 = (it0 + n % per_head) * kTileRows + 32 * hq;
+    const int qs0 = (it0 + per_head - 1 - n % per_head) * kTileRows + 32 * hq;
     // S = Q K^T, dP = dO V^T for this wavefront's 32 queries x 32 keys.
     f32x16 s, dp;
 #pragma unroll
@@ -471,13 +473,17 @@ __global__ __launch_bounds__(64 * kDkvWaves, 1) void bwd_dkdv_kernel(BwdArgs a) 
     if (n + 1 < niter) issue(n + 1, (n + 1) & 1);
     compute(n, n & 1, sb, masked);
   };
+  // Each head's query tiles are walked from the last down to the diagonal,
+  // so that the workgroups of one key/value head (all starting with the
+  // head's last tiles) read the same Q and dO tiles at about the same time
+  // and share them in their XCD's L2; the two masked tiles come last.
   const int nmask = CAUSAL ? min(2, per_head) : 0;
   issue(0, 0);
   int n = 0;
   for (int g = 0; g < group; ++g) {
     const int nend = n + per_head;
-    for (const int nm = n + nmask; n < nm; ++n) step(n, std::true_type{});
-    for (; n < nend; ++n) step(n, std::false_type{});
+    for (const int nu = nend - nmask; n < nu; ++n) step(n, std::false_type{});
+    for (; n < nend; ++n) step(n, std::true_type{});
   }
 
   // Epilogue.  Rows are staged as bf16 in LDS ([32 keys][D], 16-byte chunks
@@ -637,7 +643,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
 
   auto issue = [&](int n, int st) __attribute__((always_inline)) {
     const int g = n / per_head;
-    const int qb = (it0 + n % per_head) * kQS;
+    const int qb = (it0 + per_head - 1 - n % per_head) * kQS;
     const int h = hk * group + g;
     const int64_t qoff = qseg + (int64_t)h * q_head;
     dma_tile<D>(qdma, rows_desc(qbase + qoff, qb, len, q_row_b), sbase + SM::Q + st * SM::HT,
@@ -668,7 +674,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
     const uint16_t* dout = reinterpret_cast<const uint16_t*>(smem + SM::DO + st * SM::HT);
     const float* lse = reinterpret_cast<const float*>(smem + SM::LSE + st * (kQS * 4));
     const float* del = reinterpret_cast<const float*>(smem + SM::DEL + st * (kQS * 4));
-    const int qs0 = (it0 + n % per_head) * kQS;
+    const int qs0 = (it0 + per_head - 1 - n % per_head) * kQS;
     f32x16 s, dp;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -724,25 +730,28 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
     __syncthreads();
     if (n + 1 < niter) issue(n + 1, (n + 1) & 1);
   };
-  // Per head: under the causal mask the first four steps hold the
-  // workgroup's diagonal (masked compute, skipped by the wavefronts whose
-  // keys all follow the step's queries); the rest need no mask.  Each loop
-  // body has one form of compute (two forms in one body exceed the register
-  // budget).
+  // Per head the query steps are walked from the last down to the
+  // diagonal, so that the workgroups of one key/value head (all starting
+  // with the head's last steps) read the same Q and dO rows at about the
+  // same time and share them in their XCD's L2.  Under the causal mask the
+  // last four steps hold the workgroup's diagonal (masked compute, skipped
+  // by the wavefronts whose keys all follow the step's queries); the others
+  // need no mask.  Each loop body has one form of compute (two forms in one
+  // body exceed the register budget).
   const int ndiag = CAUSAL ? min(kKN / kQS, per_head) : 0;
   issue(0, 0);
   int n = 0;
 #pragma nounroll
   for (int g = 0; g < group; ++g) {
 #pragma nounroll
-    for (const int nd = n + ndiag; n < nd; ++n) {
+    for (const int nu = (g + 1) * per_head - ndiag; n < nu; ++n) {
       sync(n);
-      if ((it0 + n % per_head) * kQS >= kw0) compute(n, n & 1, std::true_type{});
+      compute(n, n & 1, std::false_type{});
     }
 #pragma nounroll
     for (const int ne = (g + 1) * per_head; n < ne; ++n) {
       sync(n);
-      compute(n, n & 1, std::false_type{});
+      if ((it0 + per_head - 1 - n % per_head) * kQS >= kw0) compute(n, n & 1, std::true_type{});
     }
   }
 
@@ -799,14 +808,16 @@ namespace {
 
 template <int D>
 void launch_bwd_d(const BwdArgs& a, int phases, hipStream_t stream) {
-  // One dQ workgroup per query block (see the kernel).
-  const dim3 gq((unsigned)(a.L.nseg * a.L.Hq), (unsigned)((a.L.S + kQM - 1) / kQM));
+  // One dQ workgroup per query block (see the kernel), in the XCD-aware order.
+  BwdArgs b = a;
+  b.xo = xcd_order(a.L.nseg, a.L.Hkv, a.L.group);
+  const dim3 gq((unsigned)xcd_grid(b.xo, (a.L.S + kQM - 1) / kQM));
   const dim3 gk((unsigned)(a.L.nseg * a.L.Hkv), (unsigned)((a.L.S + kKN - 1) / kKN));
   if (phases & 1) {
     if (a.causal)
-      hipLaunchKernelGGL((bwd_dq_kernel<D, true>), gq, dim3(kDqThreads), 0, stream, a);
+      hipLaunchKernelGGL((bwd_dq_kernel<D, true>), gq, dim3(kDqThreads), 0, stream, b);
     else
-      hipLaunchKernelGGL((bwd_dq_kernel<D, false>), gq, dim3(kDqThreads), 0, stream, a);
+      hipLaunchKernelGGL((bwd_dq_kernel<D, false>), gq, dim3(kDqThreads), 0, stream, b);
   }
   if (phases & 2) {
     const int form = D == 64 ? 2

@@ -58,7 +58,17 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   const int l32 = lane & 31, half = lane >> 5;
 
   const Layout L = a.L;
-  const int z = blockIdx.x / L.Hq, h = blockIdx.x % L.Hq;
+  int z, h, p;
+  if constexpr (PAGED) {
+    z = blockIdx.x / L.Hq;
+    h = blockIdx.x % L.Hq;
+    p = (int)blockIdx.y;
+  } else {
+    int gk, j;
+    if (!xcd_decode((int)blockIdx.x, a.xo, gk, j, p)) return;
+    z = gk / L.Hkv;
+    h = (gk % L.Hkv) * L.group + j;
+  }
   const int hk = h / L.group;
   const Segment seg = segment_of(L, z);
   // Keys: the segment's own rows, or (paged) its pages; the queries are the
@@ -71,7 +81,6 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
   // tiles under the causal mask start first.  Split: query block p, key
   // chunk blockIdx.z.
   const int nqt = (seg.len + kBM - 1) / kBM;
-  const int p = (int)blockIdx.y;
   const int split = PAGED ? a.split : 0;
   const int chunk = (int)blockIdx.z;
   if (p >= nqt) return;
@@ -451,12 +460,15 @@ hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream) {
       launch_merge<128>(a, mg, stream);
     return hipGetLastError();
   }
-  // One workgroup per query block (see the kernel).
-  const dim3 grid(heads, (unsigned)nqt);
-  if (a.L.kv_cu)
-    launch_fwd_p<true>(a, D, grid, stream);
-  else
-    launch_fwd_p<false>(a, D, grid, stream);
+  // One workgroup per query block (see the kernel); unpaged launches in the
+  // XCD-aware order.
+  if (a.L.kv_cu) {
+    launch_fwd_p<true>(a, D, dim3(heads, (unsigned)nqt), stream);
+  } else {
+    FwdArgs b = a;
+    b.xo = xcd_order(a.L.nseg, a.L.Hkv, a.L.group);
+    launch_fwd_p<false>(b, D, dim3((unsigned)xcd_grid(b.xo, nqt)), stream);
+  }
   return hipGetLastError();
 }
 

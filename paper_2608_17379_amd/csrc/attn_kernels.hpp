@@ -16,6 +16,41 @@
 
 namespace attn {
 
+// Order of the workgroups of a launch over (query block, query head): the
+// hardware deals workgroup ids to the chip's eight XCDs in turn (id % 8),
+// and each XCD has its own L2.  Workgroup id L is given to kv-head group
+// gk = L % 8 + 8 i (a segment's kv head with its Hq / Hkv query heads), so
+// that every query head reading one K/V head runs on one XCD and shares its
+// L2; within an XCD (ids L / 8 in dispatch order) the query blocks come
+// heaviest first (p = 0 is the block with the most key tiles), then the
+// XCD's groups, then the group's query heads.
+constexpr int kXcds = 8;
+struct XcdOrder {
+  int nkv;       // kv-head groups: segments x Hkv
+  int G;         // query heads per group
+  int per_xcd;   // groups per XCD: ceil(nkv / 8)
+};
+inline XcdOrder xcd_order(int nseg, int Hkv, int G) {
+  const int nkv = nseg * Hkv;
+  return XcdOrder{nkv, G, (nkv + kXcds - 1) / kXcds};
+}
+// Workgroups of such a launch (the last XCDs' unused slots exit at once).
+inline int64_t xcd_grid(const XcdOrder& o, int nqt) {
+  return (int64_t)kXcds * o.per_xcd * o.G * nqt;
+}
+// Workgroup L's group gk, query head j within the group and block index p;
+// false for an unused slot.
+__device__ __forceinline__ bool xcd_decode(int L, const XcdOrder& o, int& gk, int& j, int& p) {
+  const int r = L % kXcds, s = L / kXcds;
+  const int per = o.per_xcd * o.G;
+  p = s / per;
+  const int rem = s - p * per;
+  const int i = rem / o.G;
+  j = rem - i * o.G;
+  gk = r + kXcds * i;
+  return gk < o.nkv;
+}
+
 struct Layout {
   const int* cu;           // packed: cu_seqlens (device); fixed: nullptr
   int S;                   // fixed: sequence length; packed: max_seqlen
@@ -55,6 +90,7 @@ struct FwdArgs {
   int nsplit;              // chunk slots per (query row, head): the grid's z extent
   float* part_o;           // workspace [total_q, Hq, nsplit, D] fp32
   float* part_lse;         // workspace [total_q, Hq, nsplit] fp32, log2 units
+  XcdOrder xo;             // unpaged: workgroup order (set by the launcher)
 };
 
 struct BwdArgs {
@@ -74,6 +110,7 @@ struct BwdArgs {
   float scale_log2;        // scale * log2(e)
   int causal;
   int dkdv_form;           // D = 96, 128: 0 chosen by the grid, 1 one, 2 two workgroups per CU
+  XcdOrder xo;             // dQ kernel's workgroup order (set by the launcher)
 };
 
 // Paged decode: one query row per request (q, o [batch, Hq, D], lse

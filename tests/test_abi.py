@@ -303,3 +303,12 @@ def test_noalloc_validation_before_any_gpu_call():
     assert call(B=-1) == -2
     assert call(B=0, p=0) == 0   # no rows: a no-op
     assert "noalloc" in attn.attn_status_string(-9)
+
+
+def test_forward_and_dq_grid_must_fit_one_launch():
+    """The forward and dQ kernels run one 1-D grid over (query block, query
+    head) in the XCD-aware order; shapes whose grid exceeds 2^31 - 1
+    workgroups are refused before any GPU call."""
+    big_s = 128 * 65535   # the largest S check_rows allows
+    assert fwd(B=1 << 14, Hq=1 << 14, Hkv=1 << 14, S=big_s) == -2
+    assert bwd(B=1 << 14, Hq=1 << 14, Hkv=1 << 14, S=big_s) == -2

@@ -78,8 +78,8 @@ Layout packed_layout(const int* cu, int nseq, int max_seqlen, int total, int Hq,
   return L;
 }
 
-// The forward and the dQ kernel run one 1-D grid over (query block, query
-// head) in the XCD-aware order; it must fit a launch.
+// The attention kernels run 1-D grids over (block of 128 rows, head) in the
+// XCD-aware order; the largest (query heads) must fit a launch.
 bool grid_too_large(int64_t nseg, int Hq, int Hkv, int64_t rows) {
   const int64_t nkv = nseg * Hkv;
   const int64_t n = (int64_t)attn::kXcds * ((nkv + attn::kXcds - 1) / attn::kXcds) * (Hq / Hkv) *

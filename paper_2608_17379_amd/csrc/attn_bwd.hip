@@ -330,9 +330,12 @@ __global__ __launch_bounds__(64 * kDkvWaves, 1) void bwd_dkdv_kernel(BwdArgs a) 
   const int sb = wave >> 2;   // query half of each tile
 
   const Layout L = a.L;
-  const int z = blockIdx.x / L.Hkv, hk = blockIdx.x % L.Hkv;
+  int gk, j0, kb;
+  if (!xcd_decode((int)blockIdx.x, a.xk, gk, j0, kb)) return;
+  (void)j0;   // one head per group
+  const int z = gk / L.Hkv, hk = gk % L.Hkv;
   const Segment seg = segment_of(L, z);
-  const int k0 = (int)blockIdx.y * kKN;   // lowest keys (most work) first
+  const int k0 = kb * kKN;   // lowest keys (most work) first
   if (k0 >= seg.len) return;
 
   const int64_t kvoff = (int64_t)seg.start * L.kv_row + (int64_t)z * L.kv_batch +
@@ -590,9 +593,12 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
   const int kq = wave;   // 32-key group
 
   const Layout L = a.L;
-  const int z = blockIdx.x / L.Hkv, hk = blockIdx.x % L.Hkv;
+  int gk, j0, kb;
+  if (!xcd_decode((int)blockIdx.x, a.xk, gk, j0, kb)) return;
+  (void)j0;   // one head per group
+  const int z = gk / L.Hkv, hk = gk % L.Hkv;
   const Segment seg = segment_of(L, z);
-  const int k0 = (int)blockIdx.y * kKN;   // lowest keys (most work) first
+  const int k0 = kb * kKN;   // lowest keys (most work) first
   if (k0 >= seg.len) return;
 
   const int64_t kvoff = (int64_t)seg.start * L.kv_row + (int64_t)z * L.kv_batch +
@@ -810,9 +816,10 @@ template <int D>
 void launch_bwd_d(const BwdArgs& a, int phases, hipStream_t stream) {
   // One dQ workgroup per query block (see the kernel), in the XCD-aware order.
   BwdArgs b = a;
-  b.xo = xcd_order(a.L.nseg, a.L.Hkv, a.L.group);
-  const dim3 gq((unsigned)xcd_grid(b.xo, (a.L.S + kQM - 1) / kQM));
-  const dim3 gk((unsigned)(a.L.nseg * a.L.Hkv), (unsigned)((a.L.S + kKN - 1) / kKN));
+  b.xo = xcd_order(a.L.nseg, a.L.Hkv, a.L.group, (a.L.S + kQM - 1) / kQM, a.causal != 0);
+  b.xk = xcd_order(a.L.nseg, a.L.Hkv, 1, (a.L.S + kKN - 1) / kKN, a.causal != 0);
+  const dim3 gq((unsigned)xcd_grid(b.xo));
+  const dim3 gk((unsigned)xcd_grid(b.xk));
   if (phases & 1) {
     if (a.causal)
       hipLaunchKernelGGL((bwd_dq_kernel<D, true>), gq, dim3(kDqThreads), 0, stream, b);
@@ -826,16 +833,16 @@ void launch_bwd_d(const BwdArgs& a, int phases, hipStream_t stream) {
                                                    a.L.cu != nullptr, D, a.causal != 0);
     if (form == 2) {
       if (a.causal)
-        hipLaunchKernelGGL((bwd_dkdv4_kernel<D, true>), gk, dim3(256), 0, stream, a);
+        hipLaunchKernelGGL((bwd_dkdv4_kernel<D, true>), gk, dim3(256), 0, stream, b);
       else
-        hipLaunchKernelGGL((bwd_dkdv4_kernel<D, false>), gk, dim3(256), 0, stream, a);
+        hipLaunchKernelGGL((bwd_dkdv4_kernel<D, false>), gk, dim3(256), 0, stream, b);
       return;
     }
     if constexpr (D != 64) {
       if (a.causal)
-        hipLaunchKernelGGL((bwd_dkdv_kernel<D, true>), gk, dim3(64 * kDkvWaves), 0, stream, a);
+        hipLaunchKernelGGL((bwd_dkdv_kernel<D, true>), gk, dim3(64 * kDkvWaves), 0, stream, b);
       else
-        hipLaunchKernelGGL((bwd_dkdv_kernel<D, false>), gk, dim3(64 * kDkvWaves), 0, stream, a);
+        hipLaunchKernelGGL((bwd_dkdv_kernel<D, false>), gk, dim3(64 * kDkvWaves), 0, stream, b);
     }
   }
 }

@@ -466,8 +466,8 @@ hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream) {
     launch_fwd_p<true>(a, D, dim3(heads, (unsigned)nqt), stream);
   } else {
     FwdArgs b = a;
-    b.xo = xcd_order(a.L.nseg, a.L.Hkv, a.L.group);
-    launch_fwd_p<false>(b, D, dim3((unsigned)xcd_grid(b.xo, nqt)), stream);
+    b.xo = xcd_order(a.L.nseg, a.L.Hkv, a.L.group, nqt, a.causal != 0);
+    launch_fwd_p<false>(b, D, dim3((unsigned)xcd_grid(b.xo)), stream);
   }
   return hipGetLastError();
 }

@@ -16,38 +16,57 @@
 
 namespace attn {
 
-// Order of the workgroups of a launch over (query block, query head): the
-// hardware deals workgroup ids to the chip's eight XCDs in turn (id % 8),
-// and each XCD has its own L2.  Workgroup id L is given to kv-head group
-// gk = L % 8 + 8 i (a segment's kv head with its Hq / Hkv query heads), so
-// that every query head reading one K/V head runs on one XCD and shares its
-// L2; within an XCD (ids L / 8 in dispatch order) the query blocks come
-// heaviest first (p = 0 is the block with the most key tiles), then the
-// XCD's groups, then the group's query heads.
+// Order of the workgroups of a launch over (block, head): the hardware
+// deals workgroup ids to the chip's eight XCDs in turn (id % 8), and each XCD
+// has its own L2.  Workgroup id L is given to kv-head group
+// gk = L % 8 + 8 i (a segment's kv head with its G query heads, or G = 1 for
+// a launch over kv heads), so that every workgroup reading one K/V head (or
+// one group's Q and dO) runs on one XCD.  Within an XCD (ids L / 8 in
+// dispatch order) the groups come in windows of W: a window's blocks go
+// heaviest first (p = 0 has the most work under the causal mask), each
+// block for all the window's groups and their G heads side by side.  W = 1
+// (one group at a time) keeps the workgroups resident at a time on a few
+// heads' tiles in the L2; a causal launch takes windows of at least 256
+// workgroups, so that its heavy blocks are still dispatched before the
+// light ones (a window's last heavy block would otherwise start late).
 constexpr int kXcds = 8;
 struct XcdOrder {
-  int nkv;       // kv-head groups: segments x Hkv
-  int G;         // query heads per group
+  int nkv;       // groups: segments x Hkv
+  int G;         // heads per group
+  int nb;        // blocks per head (the grid's extent; a segment may have fewer)
   int per_xcd;   // groups per XCD: ceil(nkv / 8)
+  int W;         // groups per window
 };
-inline XcdOrder xcd_order(int nseg, int Hkv, int G) {
+inline XcdOrder xcd_order(int nseg, int Hkv, int G, int nb, bool causal) {
   const int nkv = nseg * Hkv;
-  return XcdOrder{nkv, G, (nkv + kXcds - 1) / kXcds};
+  const int per = (nkv + kXcds - 1) / kXcds;
+  int W = 1;
+  if (causal) {
+    const int64_t per_group = (int64_t)nb * G;
+    W = (int)((256 + per_group - 1) / per_group);
+  }
+  W = W < 1 ? 1 : (W > per ? per : W);
+  return XcdOrder{nkv, G, nb, per, W};
 }
 // Workgroups of such a launch (the last XCDs' unused slots exit at once).
-inline int64_t xcd_grid(const XcdOrder& o, int nqt) {
-  return (int64_t)kXcds * o.per_xcd * o.G * nqt;
+inline int64_t xcd_grid(const XcdOrder& o) {
+  return (int64_t)kXcds * o.per_xcd * o.G * o.nb;
 }
-// Workgroup L's group gk, query head j within the group and block index p;
-// false for an unused slot.
+// Workgroup L's group gk, head j within the group and block index p; false
+// for an unused slot.
 __device__ __forceinline__ bool xcd_decode(int L, const XcdOrder& o, int& gk, int& j, int& p) {
-  const int r = L % kXcds, s = L / kXcds;
-  const int per = o.per_xcd * o.G;
-  p = s / per;
-  const int rem = s - p * per;
-  const int i = rem / o.G;
-  j = rem - i * o.G;
-  gk = r + kXcds * i;
+  const int r = L % kXcds;
+  int s = L / kXcds;
+  const int full = o.W * o.nb * o.G;          // workgroups of a whole window
+  const int w = s / full;                     // window (the last may be short)
+  s -= w * full;
+  const int wl = min(o.W, o.per_xcd - w * o.W);   // groups in this window
+  const int per_block = wl * o.G;
+  p = s / per_block;
+  s -= p * per_block;
+  const int ig = s / o.G;
+  j = s - ig * o.G;
+  gk = r + kXcds * (w * o.W + ig);
   return gk < o.nkv;
 }
 
@@ -111,6 +130,7 @@ struct BwdArgs {
   int causal;
   int dkdv_form;           // D = 96, 128: 0 chosen by the grid, 1 one, 2 two workgroups per CU
   XcdOrder xo;             // dQ kernel's workgroup order (set by the launcher)
+  XcdOrder xk;             // dK/dV kernel's workgroup order (G = 1: kv heads)
 };
 
 // Paged decode: one query row per request (q, o [batch, Hq, D], lse

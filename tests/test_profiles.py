@@ -66,3 +66,56 @@ def test_hashed_sources_follow_includes(kernel):
                 if os.path.exists(os.path.join(csrc, inc)):
                     assert inc in files, (kernel, name, inc)
     assert "device_common.hpp" in files and "attn_kernels.hpp" in files
+
+
+def _dkdv(name):
+    w = wl.WORKLOADS[name]
+    x = wl.make_inputs(w, 0) if w.varlen else None
+    nseg = len(x.cu_seqlens) - 1 if w.varlen else w.B
+    total = x.q.shape[0] if w.varlen else 0
+    S = x.max_seqlen if w.varlen else w.S
+    # the rule of attn_bwd_dkdv_form, without loading the library: the
+    # eight-wavefront form for causal grids of fewer than 1,024 key blocks at
+    # D = 96 and 128
+    blocks = w.Hkv * (total // 128 + nseg) if w.varlen else nseg * w.Hkv * ((S + 127) // 128)
+    one = w.D != 64 and w.causal and blocks < 1024
+    return "bwd_dkdv_kernel" if one else "bwd_dkdv4_kernel"
+
+
+# Each measured workload's dominant kernel (the longest, whose roofline the
+# benchmark reports), as the kernel traces under profiles/ show.
+DOMINANT = {
+    "mha_causal_b4_h16_s2048_d128": _dkdv,
+    "gqa_causal_b2_hq32_hkv8_s4096_d128": _dkdv,
+    "long_causal_b1_h16_s16384_d128_qk2": _dkdv,
+    "varlen_causal_n8_l512_8192_h32_d64": _dkdv,
+    "ragged_gqa_causal_n33_t16294_hq32_hkv4_d128": _dkdv,
+    "mha_b4_h48_s4096_d128": _dkdv,
+    "mha_causal_b4_h48_s4096_d128": _dkdv,
+    "mha_causal_b4_h48_s4096_d96": _dkdv,
+    "paged_prefill_causal_q892_p43676_hq24_hkv8_d128": lambda n: "fwd_kernel+fwd_merge_kernel",
+    "paged_decode_b15_nnz9625_p42784_hq24_hkv8_d128": lambda n: "decode_split_kernel",
+    "gemm_bf16_nt_m8192_n7168_k5120": lambda n: "gemm_nt_kernel",
+}
+
+
+@pytest.mark.parametrize("workload", sorted(DOMINANT))
+def test_every_measured_workload_has_current_traffic(workload):
+    """The dominant kernel of every measured workload has an HBM traffic
+    record taken on the kernel's current source (so the bench line's
+    roofline.traffic is not null)."""
+    kernel = DOMINANT[workload](workload)
+    assert f"{kernel}:{workload}" in DB, kernel
+    assert bench.load_traffic(kernel, workload) is not None, (kernel, "stale source hash")
+
+
+def test_dominant_kernels_agree_with_the_traces():
+    """The dominant kernel named above is the longest attention kernel in
+    the committed trace of the workload."""
+    import re
+    for workload, fn in DOMINANT.items():
+        kernel = fn(workload).split("+")[0]
+        path = os.path.join(ROOT, "profiles", f"kernel_trace_{workload}.md")
+        rows = [l for l in open(path, encoding="utf-8") if l.startswith("| ") and "_kernel<" in l]
+        avg = {re.match(r"\| (\w+)<", l).group(1): float(l.split("|")[3]) for l in rows}
+        assert max(avg, key=avg.get) == kernel, (workload, avg)

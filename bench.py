@@ -299,8 +299,9 @@ def hold_gpu_for_enqueue(host_ms_per_step: float, steps: int) -> None:
 
 class GpuMonitor:
     """Samples the GPU's firmware metrics through amdsmi in a background
-    thread: graphics clock (MHz, mean over the XCDs), hotspot temperature (C)
-    and socket power (W).  The firmware refreshes them every few hundred
+    thread: graphics clock (MHz, mean over the XCDs), memory, fabric and SoC
+    clocks where the firmware reports them, hotspot temperature (C) and
+    socket power (W).  The firmware refreshes them every few hundred
     milliseconds, so they describe a sustained run, not a short one.
     Monitoring never fails the benchmark: without amdsmi, or when a query
     fails, the summary is None or lacks that field."""
@@ -323,6 +324,19 @@ class GpuMonitor:
             clks = [c for c in clks if isinstance(c, (int, float)) and 0 < c < 10000]
         vals = {"sclk_mhz": sum(clks) / len(clks) if clks else m.get("current_gfxclk"),
                 "temp_c": m.get("temperature_hotspot"), "power_w": m.get("current_socket_power")}
+        for key, name in (("uclk_mhz", "current_uclk"), ("fclk_mhz", "current_fclk"),
+                          ("socclk_mhz", "current_socclk")):
+            v = m.get(name)
+            if isinstance(v, list):
+                v = [c for c in v if isinstance(c, (int, float)) and 0 < c < 10000]
+                v = sum(v) / len(v) if v else None
+            vals[key] = v
+        if vals.get("fclk_mhz") is None:
+            try:   # the fabric clock's current DPM level, where the table lacks it
+                f = self._smi.amdsmi_get_clk_freq(self._h, self._smi.AmdSmiClkType.DF)
+                vals["fclk_mhz"] = f["frequency"][f["current"]] / 1e6
+            except Exception:
+                pass
         act = m.get("average_gfx_activity")
         self.samples.append((act if isinstance(act, (int, float)) else None,
                              {k: float(v) for k, v in vals.items()
@@ -367,7 +381,7 @@ class GpuMonitor:
             return None
         busy = [v for a, v in self.samples if a is not None and a >= 50]
         out = {"busy_samples": len(busy), "samples": len(self.samples)}
-        for key in ("sclk_mhz", "temp_c", "power_w"):
+        for key in ("sclk_mhz", "uclk_mhz", "fclk_mhz", "socclk_mhz", "temp_c", "power_w"):
             v = [d[key] for d in busy if key in d]
             if v:
                 out[key] = {"mean": round(sum(v) / len(v), 1), "min": min(v), "max": max(v)}

@@ -746,6 +746,12 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
   // body exceed the register budget).
   const int ndiag = CAUSAL ? min(kKN / kQS, per_head) : 0;
   issue(0, 0);
+  // Wait for every load so far (K rows, V tile, step 0) through the builtin,
+  // which the compiler's wait insertion sees (the first step waits for them
+  // anyway).  Without it the compiler takes the K-row loads as possibly
+  // outstanding inside the loop and puts vmcnt waits among the S products,
+  // which then also wait for the next step's copies, issued just before.
+  wait_vm<0>();
   int n = 0;
 #pragma nounroll
   for (int g = 0; g < group; ++g) {

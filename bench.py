@@ -92,6 +92,10 @@ METRIC = "attention fwd/bwd TFLOP/s + % bf16 MFMA peak, B4 H16 S2048 D128 causal
 GEMMS = {"fwd_kernel": 2, "bwd_dq_kernel": 1, "bwd_dkdv_kernel": 4, "bwd_dkdv4_kernel": 4}
 GEMMS_EXECUTED = {"fwd_kernel": 2, "bwd_dq_kernel": 3, "bwd_dkdv_kernel": 4,
                   "bwd_dkdv4_kernel": 4}
+# --dkdv-form names -> the attn_bwd_phases bit (include/attn.h), and each
+# bit's kernel.
+DKDV_FORMS = {"auto": 0, "one_per_cu": 4, "two_per_cu": 8}
+DKDV_KERNELS = {4: "bwd_dkdv_kernel", 8: "bwd_dkdv4_kernel"}
 RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # FLOP per byte at both roofs
 KERNEL_SOURCES = {"fwd_kernel": "attn_fwd.hip", "fwd_kernel+fwd_merge_kernel": "attn_fwd.hip",
                   "bwd_dq_kernel": "attn_bwd.hip",
@@ -774,6 +778,8 @@ def main(argv=None) -> int:
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="steps of the cold-cache pass (0: none)")
+    ap.add_argument("--dkdv-form", choices=sorted(DKDV_FORMS), default="auto",
+                    help="form of the dK/dV kernel (auto: the one the library picks)")
     ap.add_argument("--state-seconds", type=float, default=1.5,
                     help="length of the untimed pass that samples clock, temperature and power")
     args = ap.parse_args(argv)
@@ -817,6 +823,7 @@ def main(argv=None) -> int:
         lse = torch.empty(w.B, w.Hq, w.S, dtype=torch.float32, device=dev)
     ws = attn.workspace_for(q, k, cu)
     ms_len = x.max_seqlen
+    form_bit = DKDV_FORMS[args.dkdv_form]
 
     def step(ev=None):
         if ev is not None:
@@ -828,7 +835,7 @@ def main(argv=None) -> int:
                                  cu_seqlens_host=x.cu_seqlens)
         if ev is not None:
             ev[1].record()
-        for i, ph in enumerate((attn.ATTN_BWD_DQ, attn.ATTN_BWD_DKDV)):
+        for i, ph in enumerate((attn.ATTN_BWD_DQ, attn.ATTN_BWD_DKDV | form_bit)):
             if cu is None:
                 attn.attn_bwd_phases(q, k, v, o, lse, do, dq, dk, dv, w.causal, w.scale, ws, ph)
             else:
@@ -837,11 +844,15 @@ def main(argv=None) -> int:
             if ev is not None:
                 ev[2 + i].record()
 
-    # The dK/dV phase runs the form the library picks for these shapes.
+    # The dK/dV phase runs the form the library picks for these shapes, or
+    # the one --dkdv-form names.
     nseg = len(x.cu_seqlens) - 1 if w.varlen else w.B
-    form = attn.attn_bwd_dkdv_form(nseg, w.Hkv, ms_len if w.varlen else w.S,
-                                   q.shape[0] if w.varlen else 0, w.D, w.causal, w.varlen)
-    dkdv = "bwd_dkdv4_kernel" if form == attn.ATTN_BWD_DKDV_TWO_PER_CU else "bwd_dkdv_kernel"
+    form = form_bit or attn.attn_bwd_dkdv_form(nseg, w.Hkv, ms_len if w.varlen else w.S,
+                                               q.shape[0] if w.varlen else 0, w.D, w.causal,
+                                               w.varlen)
+    if w.D == 64 and form == attn.ATTN_BWD_DKDV_ONE_PER_CU:
+        form = attn.ATTN_BWD_DKDV_TWO_PER_CU   # D = 64 has no eight-wavefront form
+    dkdv = DKDV_KERNELS[form]
     kernels = ("fwd_kernel", "bwd_dq_kernel", dkdv)
     tm = time_steps(step, len(kernels), args.steps, args.warmup, args.warmup_seconds)
     ms_step, warmed = tm["ms_step"], tm["warmed"]

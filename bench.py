@@ -6,8 +6,8 @@
 Without --workload it measures the headline workload (B4 H16 S2048 D128
 causal).  The paged-cache workloads (paged prefill, paged decode) are forward
 only, as in the paper: their step is one attn_fwd_paged call (TFLOP/s; a
-prefill too small to fill the chip is split into key chunks, and the call's
-forward and merge kernels are timed together for the roofline) or one
+prefill far too small to fill the chip is split into key chunks, and the
+call's forward and merge kernels are timed together for the roofline) or one
 attn_decode_paged call (its split and merge kernels; HBM GB/s, with the
 roofline against 8 TB/s since decode reads each key and value once).  The
 GEMM workload's step is one attn_gemm_bf16_nt call (2 M N K FLOP).

@@ -221,10 +221,10 @@ int attn_bwd_varlen_phases(const void* q, const void* k, const void* v,
 
 /* Bytes of workspace for attn_fwd_paged: 0 when the prefill runs unsplit
  * (its unsplit grid of a workgroup per 128-query block, per request and
- * query head, fills the 256 CUs of the MI355X, or no request is longer
- * than 256 keys), else the partial results of the 256-key chunks: fp32
- * [total_q, Hq, ceil(max_kvlen / 256), D + 1], rounded up.  The size depends
- * on the arguments alone. */
+ * query head, fills at least half of the 256 CUs of the MI355X, or no
+ * request is longer than 256 keys), else the partial results of the
+ * 256-key chunks: fp32 [total_q, Hq, ceil(max_kvlen / 256), D + 1], rounded
+ * up.  The size depends on the arguments alone. */
 size_t attn_fwd_paged_workspace_size(int batch, int max_qlen, int total_q, int max_kvlen,
                                      int Hq, int Hkv, int D);
 
@@ -234,12 +234,14 @@ size_t attn_fwd_paged_workspace_size(int batch, int max_qlen, int total_q, int m
  * longest query run (it sizes the launch).  max_kvlen >= the largest key
  * count of a request (keys past it are ignored).  causal 0 or 1.
  *
- * When attn_fwd_paged_workspace_size is not 0 and a workspace is given (at
- * least that many bytes, 16-byte aligned, caller-owned, contents
- * irrelevant), the keys of every query block are split into chunks of 256,
- * one workgroup each, and a second kernel merges the chunks' partial
- * results, so that a few long requests still fill the device.  With a null
- * workspace the prefill runs unsplit (a non-null one that is too small is
+ * An unsplit grid with fewer workgroups than CUs runs two halves of each
+ * workgroup over alternate key tiles, combined on chip.  When
+ * attn_fwd_paged_workspace_size is not 0 and a workspace is given (at least
+ * that many bytes, 16-byte aligned, caller-owned, contents irrelevant), the
+ * keys of every query block are split into chunks of 256, one workgroup
+ * each, and a second kernel merges the chunks' partial results, so that a
+ * few long requests still fill the device.  With a null workspace the
+ * prefill runs unsplit (a non-null one that is too small is
  * ATTN_ERR_WORKSPACE).  Calls that share a workspace must not overlap.
  */
 int attn_fwd_paged(const void* q, const void* k_cache, const void* v_cache, void* o,

@@ -188,15 +188,17 @@ size_t round256(int64_t bytes) { return (size_t)((bytes + 255) / 256 * 256); }
 
 // A paged prefill whose unsplit grid (a workgroup per 128-row query block,
 // per request and query head) has fewer workgroups than the MI355X has CUs
-// is split into chunks of keys, when its requests are longer than one
-// chunk.  The rule uses the part's CU count, not a device query, so
-// that the workspace size depends on the shapes alone.
+// runs the forward's key-halves form, one 8-wavefront workgroup per CU;
+// when even that leaves more than half the CUs idle, it is split into
+// chunks of keys instead, when its requests are longer than one chunk.  The
+// rule uses the part's CU count, not a device query, so that the workspace
+// size depends on the shapes alone.
 using attn::kChipCUs;
 
 int paged_split(int batch, int max_qlen, int max_kvlen, int Hq) {
   const int64_t nqt = ((int64_t)max_qlen + attn::kFwdBlockRows - 1) / attn::kFwdBlockRows;
   const int64_t wgs = (int64_t)batch * Hq * nqt;
-  if (max_kvlen <= attn::kFwdSplitKeys || wgs >= kChipCUs) return 0;
+  if (max_kvlen <= attn::kFwdSplitKeys || wgs >= kChipCUs / 2) return 0;
   return attn::kFwdSplitKeys;
 }
 

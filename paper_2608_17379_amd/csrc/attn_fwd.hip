@@ -7,7 +7,12 @@
 //
 // Work split: one workgroup of 4 wavefronts per (segment, query head,
 // 128-row query block), the blocks with the most key tiles first, two
-// workgroups per CU; each wavefront owns 32 query rows.  The wavefront computes the transposed score tile S^T = K Q^T on
+// workgroups per CU; each wavefront owns 32 query rows.  A paged prefill
+// whose grid leaves CUs idle instead runs 8 wavefronts per block, one
+// workgroup per CU: the two halves of the workgroup take alternate key
+// tiles of the same rows, and the upper half hands its softmax state and
+// output to the lower through LDS at the end, which halves the longest
+// walk over keys without writing partial results to memory.  The wavefront computes the transposed score tile S^T = K Q^T on
 // MFMA, so lane l holds every score of query (l % 32) against half of the
 // tile's keys: the row maximum and row sum are in-lane reductions plus one
 // exchange with lane l ^ 32.  P^T, rounded to bf16, is then already laid out
@@ -42,19 +47,25 @@ constexpr float kRescaleSlack = 8.0f;   // log2 of the largest P entry allowed
 // Two LDS stages (2 x 32 KiB at D = 128 and at D = 96, whose rows are padded
 // to 128 elements; two workgroups per CU), declared as
 // separate objects so that the compiler can tell a stage being filled by DMA
-// from the one being read and does not wait for the prefetch.
+// from the one being read and does not wait for the prefetch.  With KS = 2
+// key halves each stage holds two tiles (one per half; one workgroup per CU).
 
-template <int D, bool PAGED>
-__global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
+template <int D, bool PAGED, int KS>
+__global__ __launch_bounds__(kThreads * KS, KS == 1 ? 2 : 1) void fwd_kernel(FwdArgs a) {
+  static_assert(KS == 1 || (KS == 2 && PAGED), "key halves only in the paged prefill");
   using Tile = AsyncTile<D>;
   constexpr int P = Tile::P;   // LDS row pitch (elements)
-  __shared__ __attribute__((aligned(1024))) uint16_t sk0[Tile::ELEMS];
-  __shared__ __attribute__((aligned(1024))) uint16_t sk1[Tile::ELEMS];
-  __shared__ __attribute__((aligned(1024))) uint16_t sv0[Tile::ELEMS];
-  __shared__ __attribute__((aligned(1024))) uint16_t sv1[Tile::ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t sk0[KS * Tile::ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t sk1[KS * Tile::ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t sv0[KS * Tile::ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t sv1[KS * Tile::ELEMS];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = wave_id();
+  const int lane = tid & 63, wave_all = wave_id();
+  // Row group (32 query rows) and key half of this wavefront: key tiles
+  // kt_lo + KS i + kh, i = 0, 1, ...
+  const int wave = KS == 1 ? wave_all : wave_all & 3;
+  const int kh = KS == 1 ? 0 : wave_all >> 2;
   const int l32 = lane & 31, half = lane >> 5;
 
   const Layout L = a.L;
@@ -114,10 +125,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
     // This workgroup's key tiles [kt_lo, kt_hi): all of them, or one chunk.
     // A block with no visible key has one (empty) chunk, which writes the
     // rows' O = 0 and L = -inf.
-    const int nch = split ? max(1, (kend + split - 1) / split) : 1;
+    const int nch = split && KS == 1 ? max(1, (kend + split - 1) / split) : 1;
     if (chunk >= nch) return;   // split only (unsplit grids have one z slice)
-    const int kt_lo = split ? chunk * (split / kBN) : 0;
-    const int kt_hi = split ? min(nkt, kt_lo + split / kBN) : nkt;
+    const int kt_lo = nch > 1 ? chunk * (split / kBN) : 0;
+    const int kt_hi = nch > 1 ? min(nkt, kt_lo + split / kBN) : nkt;
 
     const Tile dma(wave, lane, (int)(L.kv_row * 2));
     const RowReader<D> kr(l32, half);
@@ -157,7 +168,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
         pidx[j] = bload4(ixr, 4 * (kt * kBN + Tile::row_of(wave, j, lane)));
     };
     // Start the copies of tile kt into stages kd, vd (and, paged, the index
-    // fetch of tile kt + 1).
+    // fetch of this half's next tile, kt + KS).
     auto load_tile = [&](int kt, uint16_t* kd, uint16_t* vd) __attribute__((always_inline)) {
       if constexpr (PAGED) {
         int off[Tile::NJ];
@@ -169,7 +180,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
         }
         dma.load_at(kcache, off, kd, wave);
         dma.load_at(vcache, off, vd, wave);
-        if (kt + 1 < kt_hi) fetch(kt + 1);
+        if (kt + KS < kt_hi) fetch(kt + KS);
       } else {
         dma.load(rows_rsrc(kp, kt * kBN, kv_len, kv_row), kd, wave);
         dma.load(rows_rsrc(vp, kt * kBN, kv_len, kv_row), vd, wave);
@@ -259,14 +270,20 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
       }
       lq += lq1;
     };
-    // One tile: wait for its loads (this wavefront's, then everyone's through
-    // the barrier, which also frees the stage read one tile earlier), start the
-    // next tile's loads into that stage, then compute.
-    auto step = [&](int kt, bool work, const uint16_t* kc, const uint16_t* vc, uint16_t* kn,
+    // Step i (this half's tile kt_lo + KS i + kh, stage i % 2): wait for its
+    // loads (this wavefront's, then everyone's through the barrier, which
+    // also frees the stage read at step i - 1), start the loads of step
+    // i + 1 into that stage, then compute.
+    uint16_t* const k0s = sk0 + kh * Tile::ELEMS;
+    uint16_t* const v0s = sv0 + kh * Tile::ELEMS;
+    uint16_t* const k1s = sk1 + kh * Tile::ELEMS;
+    uint16_t* const v1s = sv1 + kh * Tile::ELEMS;
+    auto step = [&](int i, bool work, const uint16_t* kc, const uint16_t* vc, uint16_t* kn,
                     uint16_t* vn) __attribute__((always_inline)) {
       wait_vm<0>();
       __syncthreads();
-      if (kt + 1 < kt_hi) load_tile(kt + 1, kn, vn);
+      const int kt = kt_lo + KS * i + kh;
+      if (kt + KS < kt_hi) load_tile(kt + KS, kn, vn);
       if (work) compute(kt, kc, vc);
     };
 
@@ -274,32 +291,68 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdArgs a) {
     // wavefront only joins their barriers and loads.
     const int last_key = qw0 + 31 + dpos;   // the wavefront's last visible key (causal)
     const int nkt_w = causal ? (last_key < 0 ? 0 : min(kt_hi, last_key / kBN + 1)) : kt_hi;
-    if (kt_hi > kt_lo) {
-      if constexpr (PAGED) fetch(kt_lo);
-      load_tile(kt_lo, sk0, sv0);
+    // Steps of the workgroup, and those in which this wavefront computes.
+    const int nst = (kt_hi - kt_lo + KS - 1) / KS;
+    const int nst_w = nkt_w > kt_lo + kh ? (nkt_w - kt_lo - kh + KS - 1) / KS : 0;
+    if (kt_lo + kh < kt_hi) {
+      if constexpr (PAGED) fetch(kt_lo + kh);
+      load_tile(kt_lo + kh, k0s, v0s);
     }
     wait_vm<0>();   // Q rows and the first tile
-    // Tile kt uses stage kt % 2 (kt_lo is even).
-    int kt = kt_lo;
-    for (; kt + 1 < nkt_w; kt += 2) {
-      step(kt, true, sk0, sv0, sk1, sv1);
-      step(kt + 1, true, sk1, sv1, sk0, sv0);
+    int i = 0;
+    for (; i + 1 < nst_w; i += 2) {
+      step(i, true, k0s, v0s, k1s, v1s);
+      step(i + 1, true, k1s, v1s, k0s, v0s);
     }
-    if (kt < nkt_w) {
-      step(kt, true, sk0, sv0, sk1, sv1);
-      ++kt;
+    if (i < nst_w) {
+      step(i, true, k0s, v0s, k1s, v1s);
+      ++i;
     }
-    for (; kt < kt_hi; ++kt) {
-      if (kt & 1)
-        step(kt, false, sk1, sv1, sk0, sv0);
+    for (; i < nst; ++i) {
+      if (i & 1)
+        step(i, false, k1s, v1s, k0s, v0s);
       else
-        step(kt, false, sk0, sv0, sk1, sv1);
+        step(i, false, k0s, v0s, k1s, v1s);
     }
 
     // Epilogue: O = O / l, L = (m + log2 l) ln 2; or, for one chunk of
     // several, the chunk's O / l and m + log2 l (base 2) as a partial result.
     lsum += swap_halves(lsum);
     lq += swap_halves(lq);
+    if constexpr (KS == 2) {
+      // The upper half's state for the same rows and columns goes through
+      // LDS (row group w uses stage object w, now free) to the lower half,
+      // which rebases both onto the larger reference maximum and adds them.
+      __syncthreads();   // every wavefront is done with the stages
+      float* const xb = reinterpret_cast<float*>(wave == 0 ? sk0 : wave == 1 ? sk1
+                                                 : wave == 2 ? sv0 : sv1);
+      constexpr int NV = D / 2;   // output accumulator values per lane
+      static_assert((NV + 3) * 64 * 4 <= KS * Tile::ELEMS * 2, "merge staging");
+      if (kh == 1) {
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) xb[(16 * db + r) * 64 + lane] = oacc[db][r];
+        xb[NV * 64 + lane] = mref;
+        xb[(NV + 1) * 64 + lane] = lsum;
+        xb[(NV + 2) * 64 + lane] = lq;
+      }
+      __syncthreads();
+      if (kh == 1) return;
+      const float m1 = xb[NV * 64 + lane];
+      const float mnew = fmaxf(mref, m1);
+      // A half that saw no key has reference -inf and l = 0: weight 0.
+      const float a0 = mref == -INFINITY ? 0.f : fast_exp2(mref - mnew);
+      const float a1 = m1 == -INFINITY ? 0.f : fast_exp2(m1 - mnew);
+      lsum = a0 * lsum + a1 * xb[(NV + 1) * 64 + lane];
+      lq = a0 * lq + a1 * xb[(NV + 2) * 64 + lane];
+      mref = mnew;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          oacc[db][r] = a0 * oacc[db][r] + a1 * xb[(16 * db + r) * 64 + lane];
+    }
     if (nch > 1) {
       if (qrow < seg.len) {
         const float inv = lq > 0.f ? 1.f / lq : 0.f;
@@ -421,26 +474,30 @@ template __global__ void fwd_merge_kernel<128>(FwdArgs);
 
 // Explicit instantiations: without them the host compiler may skip the
 // launch stubs of these templates (leaving undefined symbols in the library).
-template __global__ void fwd_kernel<64, false>(FwdArgs);
-template __global__ void fwd_kernel<96, false>(FwdArgs);
-template __global__ void fwd_kernel<128, false>(FwdArgs);
-template __global__ void fwd_kernel<64, true>(FwdArgs);
-template __global__ void fwd_kernel<96, true>(FwdArgs);
-template __global__ void fwd_kernel<128, true>(FwdArgs);
+template __global__ void fwd_kernel<64, false, 1>(FwdArgs);
+template __global__ void fwd_kernel<96, false, 1>(FwdArgs);
+template __global__ void fwd_kernel<128, false, 1>(FwdArgs);
+template __global__ void fwd_kernel<64, true, 1>(FwdArgs);
+template __global__ void fwd_kernel<96, true, 1>(FwdArgs);
+template __global__ void fwd_kernel<128, true, 1>(FwdArgs);
+template __global__ void fwd_kernel<64, true, 2>(FwdArgs);
+template __global__ void fwd_kernel<96, true, 2>(FwdArgs);
+template __global__ void fwd_kernel<128, true, 2>(FwdArgs);
 
 template <int D>
 void launch_merge(const FwdArgs& a, dim3 grid, hipStream_t stream) {
   hipLaunchKernelGGL((fwd_merge_kernel<D>), grid, dim3(256), 0, stream, a);
 }
 
-template <bool PAGED>
+template <bool PAGED, int KS = 1>
 void launch_fwd_p(const FwdArgs& a, int D, dim3 grid, hipStream_t stream) {
+  const dim3 block(kThreads * KS);
   if (D == 64)
-    hipLaunchKernelGGL((fwd_kernel<64, PAGED>), grid, dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL((fwd_kernel<64, PAGED, KS>), grid, block, 0, stream, a);
   else if (D == 96)
-    hipLaunchKernelGGL((fwd_kernel<96, PAGED>), grid, dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL((fwd_kernel<96, PAGED, KS>), grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL((fwd_kernel<128, PAGED>), grid, dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL((fwd_kernel<128, PAGED, KS>), grid, block, 0, stream, a);
 }
 
 }  // namespace
@@ -461,9 +518,13 @@ hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream) {
     return hipGetLastError();
   }
   // One workgroup per query block (see the kernel); unpaged launches in the
-  // XCD-aware order.
+  // XCD-aware order.  A paged grid with fewer workgroups than CUs runs the
+  // 8-wavefront form (key halves), one workgroup per CU.
   if (a.L.kv_cu) {
-    launch_fwd_p<true>(a, D, dim3(heads, (unsigned)nqt), stream);
+    if ((int64_t)heads * nqt < kChipCUs)
+      launch_fwd_p<true, 2>(a, D, dim3(heads, (unsigned)nqt), stream);
+    else
+      launch_fwd_p<true>(a, D, dim3(heads, (unsigned)nqt), stream);
   } else {
     FwdArgs b = a;
     b.xo = xcd_order(a.L.nseg, a.L.Hkv, a.L.group, nqt, a.causal != 0);

@@ -207,7 +207,10 @@ def test_paged_prefill_workspace_size():
         (slots * 4 + 255) // 256 * 256
     assert size(2, 64, 100, 256, 4, 2, 128) == 0         # one chunk: no split
     assert size(64, 4096, 64 * 4096, 4096, 32, 8, 128) == 0   # the grid fills the chip
-    assert size(1, 892, 892, 892, 24, 8, 128) > 0        # the paper's paged prefill
+    # the paper's paged prefill: 7 blocks x 24 heads = 168 workgroups, fewer
+    # than the 256 CUs but more than half: the key-halves form, no split
+    assert size(1, 892, 892, 892, 24, 8, 128) == 0
+    assert size(1, 640, 640, 892, 24, 8, 128) > 0        # 5 x 24 = 120 < 128: split
     assert size(0, 64, 100, 600, 4, 2, 128) == 0
     assert size(2, 64, 100, 0, 4, 2, 128) == 0
 

@@ -5,11 +5,16 @@ attn_decode_paged, called through the C ABI by the binding.
 Small cases span several key tiles (64 keys forward), several decode chunks
 (64 keys) and ragged tails, with head dimensions 64, 96 and 128, grouped
 query heads, requests with fewer queries than keys, and empty requests.
-Paged prefill runs both ways: split into 256-key chunks with a merge (what
-the library does when the grid is small, as in every case here) and
-unsplit (no workspace); the split cases include blocks of one to four
-chunks and ragged last chunks.  The paper's two paged workloads run at full
-size, compared on every head.
+Paged prefill runs in each of its three forms: split into 256-key chunks
+with a merge (what the library does, given a workspace, when the unsplit
+grid would leave more than half the CUs idle: the two-head cases here),
+the 8-wavefront key-halves form (an unsplit grid with fewer workgroups
+than CUs: the two-head cases without a workspace, and the paper's prefill)
+and the plain unsplit form (the six-head cases, 288 workgroups).  The
+split cases include blocks of one to four chunks and ragged last chunks;
+the key-halves cases include requests whose keys all fall in one tile (one
+half sees none) and rows that see no key.  The paper's two paged workloads
+run at full size, compared on every head.
 """
 import pytest
 import torch

@@ -155,7 +155,7 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
         for (int w = 0; w < 4; ++w)
           dsum += bf16_lo(doreg[c][w]) * bf16_lo(ov[c][w]) + bf16_hi(doreg[c][w]) * bf16_hi(ov[c][w]);
     }
-    const float delta = dsum + swap_halves(dsum);
+    const float delta = sum_halves(dsum);
     if (valid && half == 0) {
       a.delta[roff + qrow] = delta;
       a.lse2[roff + qrow] = lse2;

@@ -111,7 +111,7 @@ __global__ __launch_bounds__(64) void decode_split_kernel(DecodeArgs a) {
       s[b][r] = key < len ? s[b][r] : -INFINITY;
       mx = fmaxf(mx, s[b][r]);
     }
-  mx = fmaxf(mx, swap_halves(mx));
+  mx = max_halves(mx);
   const float mt = mx * a.scale_log2;   // the chunk's row maximum, exp2 units (finite)
   float ls = 0.f;
 #pragma unroll
@@ -121,7 +121,7 @@ __global__ __launch_bounds__(64) void decode_split_kernel(DecodeArgs a) {
       s[b][r] = fast_exp2(__builtin_fmaf(s[b][r], a.scale_log2, -mt));
       ls += s[b][r];
     }
-  ls += swap_halves(ls);
+  ls = sum_halves(ls);
 
   // O^T[d][q] = sum over the chunk's keys of V^T[d][key] P^T[key][q], V^T
   // read transposed out of the V tile (chunk c of block b = tile rows

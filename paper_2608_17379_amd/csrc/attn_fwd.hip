@@ -216,7 +216,7 @@ __global__ __launch_bounds__(kThreads * KS, KS == 1 ? 2 : 1) void fwd_kernel(Fwd
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-      mx = fmaxf(mx, swap_halves(mx));
+      mx = max_halves(mx);
       const float mt = mx * sl2;   // this tile's row max in exp2 units
       if (__ballot(mt > mref + kRescaleSlack)) {
         const float mnew = fmaxf(mref, mt);
@@ -317,8 +317,8 @@ __global__ __launch_bounds__(kThreads * KS, KS == 1 ? 2 : 1) void fwd_kernel(Fwd
 
     // Epilogue: O = O / l, L = (m + log2 l) ln 2; or, for one chunk of
     // several, the chunk's O / l and m + log2 l (base 2) as a partial result.
-    lsum += swap_halves(lsum);
-    lq += swap_halves(lq);
+    lsum = sum_halves(lsum);
+    lq = sum_halves(lq);
     if constexpr (KS == 2) {
       // The upper half's state for the same rows and columns goes through
       // LDS (row group w uses stage object w, now free) to the lower half,

@@ -55,8 +55,21 @@ __device__ __forceinline__ u32x4 pack_chunk(const f32x16& x, int c) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Value of the partner lane l ^ 32 (the other half of the wavefront).
-__device__ __forceinline__ float swap_halves(float x) { return __shfl_xor(x, 32); }
+// Maximum and sum of x over the lane pair (l, l ^ 32), the same on both
+// lanes.  v_permlane32_swap exchanges the two halves of the wavefront in the
+// vector ALU (no LDS round trip, as a cross-lane shuffle would take); its
+// two results hold the pair's two values, one each, so a symmetric
+// combination of them is the pair's.
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 __device__ __forceinline__ u32x4 ld16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(uint16_t* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }

@@ -199,6 +199,19 @@ __global__ __launch_bounds__(kThreads * KS, KS == 1 ? 2 : 1) void fwd_kernel(Fwd
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
           s[kb] = mfma32(ld16(kt_lds + kr.rm[c] + 32 * kb * P), qreg[c], s[kb]);
+      // Keep the K operand reads several MFMAs ahead of their products (left
+      // to itself, the scheduler issues them one or two ahead, so most of the
+      // S products wait out an LDS read).
+      {
+        constexpr int NR = D / 8, LEAD = NR < 6 ? NR : 6;
+        __builtin_amdgcn_sched_group_barrier(0x100, LEAD, 0);   // LDS reads
+#pragma unroll
+        for (int i = 0; i < NR - LEAD; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, LEAD, 0);
+      }
 
       // s[kb][r] is the raw score of key k0 + 32kb + 8(r/4) + 4half + r%4.
       if ((a.causal && k0 + kBN - 1 > qw0 + dpos) || k0 + kBN > kv_len) {

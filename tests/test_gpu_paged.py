@@ -9,8 +9,9 @@ Paged prefill runs in each of its three forms: split into 256-key chunks
 with a merge (what the library does, given a workspace, when the unsplit
 grid would leave more than half the CUs idle: the two-head cases here),
 the 8-wavefront key-halves form (an unsplit grid with fewer workgroups
-than CUs: the two-head cases without a workspace, and the paper's prefill)
-and the plain unsplit form (the six-head cases, 288 workgroups).  The
+than CUs: the two-head cases without a workspace, the grouped four-head
+cases, 192 workgroups, either way, and the paper's prefill) and the plain
+unsplit form (the six-head cases, 288 workgroups).  The
 split cases include blocks of one to four chunks and ragged last chunks;
 the key-halves cases include requests whose keys all fall in one tile (one
 half sees none) and rows that see no key.  The paper's two paged workloads
@@ -74,7 +75,7 @@ def _prefill(q, kc, vc, qo, kv, idx, causal, scale, label, split=True):
 @pytest.mark.parametrize("split", [True, False])
 @pytest.mark.parametrize("D", [64, 96, 128])
 @pytest.mark.parametrize("causal", [False, True])
-@pytest.mark.parametrize("Hq,Hkv", [(2, 2), (6, 2)])
+@pytest.mark.parametrize("Hq,Hkv", [(2, 2), (4, 2), (6, 2)])
 def test_paged_prefill(D, causal, Hq, Hkv, split):
     # q_len == kv_len, q_len < kv_len (a continued prefill), one key, a
     # request with more queries than keys, an empty request, a request of

@@ -16,8 +16,10 @@
 //
 // With one workgroup per CU the tiles run in rounds of one per CU; when the
 // last round would be at most half full, its tiles are computed as 128-row
-// halves by a second launch (8 wavefronts of 64 x 64 each), which fills the
-// chip for half a round instead of half the chip for a whole one.
+// halves (8 wavefronts of 64 x 64 each), which fills the chip for half a
+// round instead of half the chip for a whole one.  Such a call is one launch
+// of one workgroup per CU that runs its full tiles and then its half tile
+// (gemm_rounds_kernel); any other runs one workgroup per tile.
 //
 // Tiles are assigned XCD by XCD: the hardware hands workgroup ids to the 8
 // XCDs in turn, so workgroup b runs on XCD b % 8; the tiles are numbered so
@@ -45,31 +47,23 @@ static_assert(kTK / 16 == 4, "one 64-row sub-tile copied per 16-wide K chunk");
 constexpr int kSubElems = GTile::ELEMS;            // 4096 bf16
 constexpr int kTileElems = 4 * kSubElems;          // 256 rows
 
-// TM = 256: workgroup b computes tile g.tile0 + b (in the order below).
-// TM = 128: workgroups 2 i and 2 i + 1 compute the two 128-row halves of
-// tile g.tile0 + i.
+// Tile t of the tile order (TM = 256), or its 128-row half hm (TM = 128),
+// by the whole workgroup, on the LDS stages (sa0, sb0) and (sa1, sb1).
 template <int TM, bool KTAIL>
-__global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs g) {
+__device__ __forceinline__ void gemm_tile(const GemmArgs& g, int t, int hm, uint16_t* sa0,
+                                          uint16_t* sb0, uint16_t* sa1, uint16_t* sb1) {
   constexpr int ASUB = TM / 64;   // 64-row sub-tiles of the A tile
   constexpr int MB = TM / 64;     // 32-row blocks of each wavefront (4 or 2)
   constexpr int NB = 2;           // 32-column blocks of each wavefront
-  __shared__ __attribute__((aligned(1024))) uint16_t sa0[ASUB * kSubElems];
-  __shared__ __attribute__((aligned(1024))) uint16_t sb0[kTileElems];
-  __shared__ __attribute__((aligned(1024))) uint16_t sa1[ASUB * kSubElems];
-  __shared__ __attribute__((aligned(1024))) uint16_t sb1[kTileElems];
 
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int l32 = lane & 31, half = lane >> 5;
 
-  // Tile of this workgroup.
-  const int nblk = (int)gridDim.x, bid = (int)blockIdx.x;
-  const int w = nblk % 8 == 0 ? (bid % 8) * (nblk / 8) + bid / 8 : bid;
-  const int t = g.tile0 + (TM == kTM ? w : w / 2);
   const int band_tiles = kBand * g.tiles_n;
   const int m_first = (t / band_tiles) * kBand;
   const int band_rows = min(kBand, g.tiles_m - m_first);
   const int tb = t % band_tiles;
-  const int m0 = (m_first + tb % band_rows) * kTM + (TM == kTM ? 0 : (w % 2) * TM);
+  const int m0 = (m_first + tb % band_rows) * kTM + hm * TM;
   const int n0 = (tb / band_rows) * kTN;
 
   const int K = g.K;
@@ -174,6 +168,58 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs g) {
   }
 }
 
+// TM = 256: workgroup b computes tile g.tile0 + b (in the order below).
+// TM = 128: workgroups 2 i and 2 i + 1 compute the two 128-row halves of
+// tile g.tile0 + i.
+template <int TM, bool KTAIL>
+__global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs g) {
+  constexpr int ASUB = TM / 64;
+  __shared__ __attribute__((aligned(1024))) uint16_t sa0[ASUB * kSubElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sb0[kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sa1[ASUB * kSubElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sb1[kTileElems];
+  const int nblk = (int)gridDim.x, bid = (int)blockIdx.x;
+  const int w = nblk % 8 == 0 ? (bid % 8) * (nblk / 8) + bid / 8 : bid;
+  gemm_tile<TM, KTAIL>(g, g.tile0 + (TM == kTM ? w : w / 2), TM == kTM ? 0 : w % 2, sa0, sb0,
+                       sa1, sb1);
+}
+
+// The whole call in one launch of one workgroup per CU (gridDim.x, a
+// multiple of 8 that divides full): the first full tiles in rounds, each
+// workgroup taking the tiles that workgroups bid, bid + gridDim.x, ... of
+// gemm_nt_kernel<256> would take (so the XCD of every tile is the same),
+// then the 128-row halves of the remaining tiles, as the workgroups of
+// gemm_nt_kernel<128> would take them.  Each workgroup thus runs its last
+// round's half tile right after its full tiles, with no second launch.
+struct RoundsArgs {
+  GemmArgs g;
+  int full;   // tiles run whole, in rounds (a multiple of gridDim.x)
+};
+
+template <bool KTAIL>
+__global__ __launch_bounds__(kThreads, 1) void gemm_rounds_kernel(RoundsArgs args) {
+  const GemmArgs& g = args.g;
+  __shared__ __attribute__((aligned(1024))) uint16_t sa0[kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sb0[kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sa1[kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sb1[kTileElems];
+  const int nblk = (int)gridDim.x, bid = (int)blockIdx.x;
+  const int x = bid % 8, j = bid / 8, per = nblk / 8;
+  const int full = args.full;
+  const int rounds = full / nblk;
+  for (int r = 0; r < rounds; ++r) {
+    gemm_tile<kTM, KTAIL>(g, x * (full / 8) + j + per * r, 0, sa0, sb0, sa1, sb1);
+    __syncthreads();   // every wavefront is done with the stages
+  }
+  const int nhalf = 2 * (g.tiles_m * g.tiles_n - full);
+  if (bid < nhalf) {
+    const int w = nhalf % 8 == 0 ? x * (nhalf / 8) + j : bid;
+    gemm_tile<128, KTAIL>(g, full + w / 2, w % 2, sa0, sb0, sa1, sb1);
+  }
+}
+
+template __global__ void gemm_rounds_kernel<false>(RoundsArgs);
+template __global__ void gemm_rounds_kernel<true>(RoundsArgs);
 template __global__ void gemm_nt_kernel<256, false>(GemmArgs);
 template __global__ void gemm_nt_kernel<256, true>(GemmArgs);
 template __global__ void gemm_nt_kernel<128, false>(GemmArgs);
@@ -200,6 +246,17 @@ hipError_t launch_gemm(const GemmArgs& g, int cus, hipStream_t stream) {
   const int tiles = g.tiles_m * g.tiles_n;
   const int rem = cus > 0 ? tiles % cus : 0;
   const bool split = tiles > cus && rem > 0 && 2 * rem <= cus;
+  if (split && cus % 8 == 0) {
+    // Both parts in one launch of one workgroup per CU.
+    const RoundsArgs r{g, tiles - rem};
+    if (g.K % kTK != 0)
+      hipLaunchKernelGGL((gemm_rounds_kernel<true>), dim3((unsigned)cus), dim3(kThreads), 0,
+                         stream, r);
+    else
+      hipLaunchKernelGGL((gemm_rounds_kernel<false>), dim3((unsigned)cus), dim3(kThreads), 0,
+                         stream, r);
+    return hipGetLastError();
+  }
   GemmArgs full = g;
   full.tile0 = 0;
   launch_part<kTM>(full, split ? tiles - rem : tiles, stream);

@@ -95,7 +95,7 @@ DOMINANT = {
     "mha_causal_b4_h48_s4096_d96": _dkdv,
     "paged_prefill_causal_q892_p43676_hq24_hkv8_d128": lambda n: "fwd_kernel",
     "paged_decode_b15_nnz9625_p42784_hq24_hkv8_d128": lambda n: "decode_split_kernel",
-    "gemm_bf16_nt_m8192_n7168_k5120": lambda n: "gemm_nt_kernel",
+    "gemm_bf16_nt_m8192_n7168_k5120": lambda n: "gemm_rounds_kernel",
 }
 
 

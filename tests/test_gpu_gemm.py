@@ -59,9 +59,12 @@ def _draw(seed, M, N, K):
 @pytest.mark.parametrize("M,N,K", [(1, 8, 8), (256, 256, 64), (255, 264, 72), (300, 520, 200),
                                    (513, 1000, 1024), (64, 2048, 136), (1024, 256, 5120),
                                    (2048, 2048, 512),
-                                   # more tiles than CUs with a small last round: that
-                                   # round runs as 128-row half tiles (ragged M, K tail)
-                                   (4252, 4096, 136)])
+                                   # more tiles than CUs with a small last round: one
+                                   # launch runs the full tiles in rounds, then that
+                                   # round as 128-row half tiles (ragged M, K tail;
+                                   # ragged N; 3 half-tiled tiles, whose 6 halves do
+                                   # not divide among the 8 XCDs)
+                                   (4252, 4096, 136), (4352, 4072, 520), (1792, 9472, 64)])
 def test_gemm_shapes(M, N, K):
     a, b = _draw(M + N + K, M, N, K)
     announce(f"gemm M={M} N={N} K={K}")

@@ -766,6 +766,53 @@ def copy_calibration(nbytes: int, reps: int) -> None:
     print(json.dumps({"copy_bytes": nbytes, "reps": reps}), flush=True)
 
 
+def mfma_calibration(iters: int, reps: int, seconds: float) -> None:
+    """The chip's sustained bf16 MFMA rate: two 4-wavefront workgroups per CU
+    running independent chains of v_mfma_f32_32x32x16_bf16 on registers
+    (libcalib.so), timed by events, with the graphics clock sampled over a
+    sustained pass.  flop/clk/CU = rate / (CUs x clock); the quoted peak
+    assumes 4096 at 2.4 GHz."""
+    import ctypes
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_17379_amd", "libcalib.so"))
+    lib.calib_mfma_rate.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    chains = lib.calib_mfma_chains()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks = 2 * cus
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def launch():
+        st = lib.calib_mfma_rate(blocks, iters, ctypes.c_void_p(out.data_ptr()),
+                                 ctypes.c_void_p(stream))
+        if st != 0:
+            raise RuntimeError(f"calib_mfma_rate returned {st}")
+
+    for _ in range(3):
+        launch()
+    state = sustained_state(launch, seconds)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        launch()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    flop = float(blocks) * 4 * iters * chains * 32768
+    tflops = flop / (ms * 1e-3) / 1e12
+    rec = {"mfma_calibration": {"blocks": blocks, "wavefronts_per_simd": 2, "iters": iters,
+                                "chains": chains, "ms_per_launch": round(ms, 4),
+                                "tflops": round(tflops, 1), "cus": cus,
+                                "frac_of_quoted_peak": round(tflops / PEAK_BF16_TFLOPS, 4)}}
+    sclk = (state or {}).get("sclk_mhz", {}).get("mean") if state else None
+    if sclk:
+        rec["mfma_calibration"]["sclk_mhz"] = sclk
+        rec["mfma_calibration"]["flop_per_clk_per_cu"] = round(
+            tflops * 1e12 / (cus * sclk * 1e6), 1)
+    rec["gpu_state"] = state
+    print(json.dumps(rec), flush=True)
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -778,6 +825,8 @@ def main(argv=None) -> int:
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
+    ap.add_argument("--mfma-calibration", type=int, default=0, metavar="ITERS",
+                    help="measure the sustained MFMA rate (ITERS loop trips per wavefront)")
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="steps of the cold-cache pass (0: none)")
     ap.add_argument("--dkdv-form", choices=sorted(DKDV_FORMS), default="auto",
@@ -800,6 +849,9 @@ def main(argv=None) -> int:
         return 1
     if args.copy_calibration:
         copy_calibration(args.copy_calibration, max(1, args.steps))
+        return 0
+    if args.mfma_calibration:
+        mfma_calibration(args.mfma_calibration, max(1, args.steps), args.state_seconds)
         return 0
 
     name = args.workload or wl.HEADLINE

@@ -315,3 +315,16 @@ def test_forward_and_dq_grid_must_fit_one_launch():
     big_s = 128 * 65535   # the largest S check_rows allows
     assert fwd(B=1 << 14, Hq=1 << 14, Hkv=1 << 14, S=big_s) == -2
     assert bwd(B=1 << 14, Hq=1 << 14, Hkv=1 << 14, S=big_s) == -2
+
+
+def test_calibration_library_exports():
+    """The benchmark's MFMA-rate calibration library (measurement support,
+    not part of the attention ABI) is built beside libattn.so and exports
+    its two entry points."""
+    path = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                        "paper_2608_17379_amd", "libcalib.so")
+    lib = ctypes.CDLL(path)
+    for name in ("calib_mfma_rate", "calib_mfma_chains"):
+        assert hasattr(lib, name), name
+    assert lib.calib_mfma_chains() == 8
+

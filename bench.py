@@ -621,10 +621,14 @@ def run_paged(args, w) -> int:
             attn.attn_decode_paged_phases(q, kc, vc, o, lse, kv, idx, x.max_kvlen, w.scale, ws,
                                           ph, **host)
     else:
-        # A prefill too small to fill the chip runs split (two kernels in one
-        # call, timed together).
+        # The call is given the workspace it asks for.  A prefill far too small
+        # to fill the chip then runs split (two kernels in one call, timed
+        # together); one that leaves CUs idle runs the key-halves form.
         ws = attn.prefill_workspace_for(q, kc, w.batch, x.max_qlen, x.max_kvlen)
         kernels = ("fwd_kernel+fwd_merge_kernel",) if ws is not None else ("fwd_kernel",)
+        form = {attn.ATTN_FWD_PAGED_UNSPLIT: "unsplit", attn.ATTN_FWD_PAGED_KEY_HALVES: "key halves",
+                attn.ATTN_FWD_PAGED_SPLIT: "split"}[
+            attn.attn_fwd_paged_form(w.batch, x.max_qlen, x.max_kvlen, w.Hq, True)]
 
         def launch(i):
             attn.attn_fwd_paged(q, kc, vc, o, lse, qo, kv, idx, x.max_qlen, x.max_kvlen,
@@ -651,6 +655,8 @@ def run_paged(args, w) -> int:
            "nnz": w.nnz, "num_pages": w.num_pages, "page_size": 1, "causal": w.causal,
            "decode": w.decode, "seed": 0,
            "kv_lens": [b - a for a, b in zip(x.kv_indptr, x.kv_indptr[1:])]}
+    if not w.decode:
+        cfg["prefill_form"] = form
     rec = {"n_gpus": 1, "steps": args.steps, "warmup": warmed, "warmup_requested": args.warmup,
            "warmup_seconds": args.warmup_seconds,
            "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",

@@ -228,6 +228,26 @@ int attn_bwd_varlen_phases(const void* q, const void* k, const void* v,
 size_t attn_fwd_paged_workspace_size(int batch, int max_qlen, int total_q, int max_kvlen,
                                      int Hq, int Hkv, int D);
 
+/* The form attn_fwd_paged runs for these arguments (with_workspace 1: a
+ * workspace of attn_fwd_paged_workspace_size bytes is passed; 0: none).  No
+ * GPU call.
+ *   ATTN_FWD_PAGED_UNSPLIT     one 4-wavefront workgroup per 128-query block
+ *                              (the unsplit grid fills the 256 CUs);
+ *   ATTN_FWD_PAGED_KEY_HALVES  one 8-wavefront workgroup per block, whose two
+ *                              halves take alternate key tiles and combine on
+ *                              chip (an unsplit grid of fewer workgroups than
+ *                              CUs);
+ *   ATTN_FWD_PAGED_SPLIT       256-key chunks, one workgroup each, then a merge
+ *                              kernel (a workspace, a request longer than 256
+ *                              keys, and an unsplit grid of fewer than 128
+ *                              workgroups).
+ * Returns ATTN_ERR_SHAPE for batch, max_qlen or Hq below 1, max_kvlen below
+ * 0 or batch * Hq above 2^30, ATTN_ERR_VALUE for another with_workspace. */
+#define ATTN_FWD_PAGED_UNSPLIT 0
+#define ATTN_FWD_PAGED_KEY_HALVES 1
+#define ATTN_FWD_PAGED_SPLIT 2
+int attn_fwd_paged_form(int batch, int max_qlen, int max_kvlen, int Hq, int with_workspace);
+
 /*
  * Paged prefill.  q, o [total_q, Hq, D] packed by qo_indptr (int32 [batch+1],
  * from 0 to total_q, as cu_seqlens); lse [Hq, total_q] fp32.  max_qlen >= the

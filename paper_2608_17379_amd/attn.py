@@ -27,7 +27,7 @@ EXPORTS = ("attn_fwd", "attn_bwd", "attn_bwd_workspace_size", "attn_fwd_varlen",
            "attn_bwd_varlen", "attn_bwd_varlen_workspace_size", "attn_bwd_phases",
            "attn_bwd_noalloc",
            "attn_bwd_varlen_phases", "attn_bwd_dkdv_form", "attn_fwd_paged_workspace_size",
-           "attn_fwd_paged",
+           "attn_fwd_paged_form", "attn_fwd_paged",
            "attn_decode_paged_workspace_size",
            "attn_decode_paged", "attn_decode_paged_phases", "attn_gemm_bf16_nt",
            "attn_status_string")
@@ -35,6 +35,9 @@ ATTN_BWD_DQ = 1
 ATTN_BWD_DKDV = 2
 ATTN_BWD_DKDV_ONE_PER_CU = 4
 ATTN_BWD_DKDV_TWO_PER_CU = 8
+ATTN_FWD_PAGED_UNSPLIT = 0
+ATTN_FWD_PAGED_KEY_HALVES = 1
+ATTN_FWD_PAGED_SPLIT = 2
 ATTN_DECODE_SPLIT = 1
 ATTN_DECODE_MERGE = 2
 ATTN_BWD_NOALLOC_SCRATCH_BYTES = 16 << 20
@@ -79,6 +82,8 @@ def lib() -> ctypes.CDLL:
         l.attn_bwd_dkdv_form.restype = _I
         l.attn_fwd_paged_workspace_size.argtypes = [_I] * 7
         l.attn_fwd_paged_workspace_size.restype = _Z
+        l.attn_fwd_paged_form.argtypes = [_I] * 5
+        l.attn_fwd_paged_form.restype = _I
         l.attn_fwd_paged.argtypes = [_P] * 8 + [_I] * 10 + [_F, _P, _Z, _P]
         l.attn_fwd_paged.restype = _I
         l.attn_decode_paged_workspace_size.argtypes = [_I] * 5
@@ -412,6 +417,16 @@ def gemm_nt(a, b):
 # --------------------------------------------------------------------------
 # Allocating conveniences (torch allocates the outputs; the library fills them)
 # --------------------------------------------------------------------------
+
+def attn_fwd_paged_form(batch: int, max_qlen: int, max_kvlen: int, Hq: int,
+                        with_workspace: bool) -> int:
+    """The form attn_fwd_paged runs (ATTN_FWD_PAGED_UNSPLIT, _KEY_HALVES or
+    _SPLIT) for these shapes, with or without a workspace."""
+    st = lib().attn_fwd_paged_form(batch, max_qlen, max_kvlen, Hq, int(bool(with_workspace)))
+    if st < 0:
+        _check(st, "attn_fwd_paged_form")
+    return st
+
 
 def prefill_workspace_for(q, k_cache, batch: int, max_qlen: int, max_kvlen: int):
     """The workspace attn_fwd_paged needs for these shapes, or None when it

@@ -392,6 +392,16 @@ size_t attn_fwd_paged_workspace_size(int batch, int max_qlen, int total_q, int m
   return round256(slots * D * 4) + round256(slots * 4);
 }
 
+int attn_fwd_paged_form(int batch, int max_qlen, int max_kvlen, int Hq, int with_workspace) {
+  if (batch < 1 || max_qlen < 1 || max_kvlen < 0 || Hq < 1) return ATTN_ERR_SHAPE;
+  if ((int64_t)batch * Hq > (int64_t)1 << 30) return ATTN_ERR_SHAPE;
+  if (with_workspace != 0 && with_workspace != 1) return ATTN_ERR_VALUE;
+  if (with_workspace && paged_split(batch, max_qlen, max_kvlen, Hq) > 0)
+    return ATTN_FWD_PAGED_SPLIT;
+  return attn::paged_key_halves((int64_t)batch * Hq, max_qlen) ? ATTN_FWD_PAGED_KEY_HALVES
+                                                                : ATTN_FWD_PAGED_UNSPLIT;
+}
+
 int attn_fwd_paged(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse,
                    const int* qo_indptr, const int* kv_indptr, const int* kv_indices, int batch,
                    int max_qlen, int total_q, int max_kvlen, int nnz, int num_pages, int Hq,

@@ -534,7 +534,7 @@ hipError_t launch_fwd(const FwdArgs& a, int D, hipStream_t stream) {
   // XCD-aware order.  A paged grid with fewer workgroups than CUs runs the
   // 8-wavefront form (key halves), one workgroup per CU.
   if (a.L.kv_cu) {
-    if ((int64_t)heads * nqt < kChipCUs)
+    if (paged_key_halves(heads, a.L.S))
       launch_fwd_p<true, 2>(a, D, dim3(heads, (unsigned)nqt), stream);
     else
       launch_fwd_p<true>(a, D, dim3(heads, (unsigned)nqt), stream);

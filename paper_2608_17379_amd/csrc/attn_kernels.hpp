@@ -171,6 +171,14 @@ constexpr int kDecodeChunk = 64;
 constexpr int kChipCUs = 256;        // compute units of the MI355X
 constexpr int kFwdSplitKeys = 256;   // keys per chunk of a split paged prefill
 constexpr int kFwdBlockRows = 128;   // query rows per forward workgroup
+
+// An unsplit paged prefill runs the forward's 8-wavefront key-halves form
+// when its grid (a workgroup per 128-query block, per request and query
+// head: `heads` = requests x query heads) has fewer workgroups than the
+// chip has CUs.
+inline bool paged_key_halves(int64_t heads, int max_qlen) {
+  return heads * ((max_qlen + kFwdBlockRows - 1) / kFwdBlockRows) < kChipCUs;
+}
 // phases: bit 0 = split kernel, bit 1 = merge kernel.
 hipError_t launch_decode(const DecodeArgs& a, int D, int phases, hipStream_t stream);
 // phases: bit 0 = Delta and dQ kernel, bit 1 = dK/dV kernel.

@@ -199,6 +199,29 @@ def test_paged_prefill_specific_validation():
     assert fwdp(wsb=1 << 30, ws=A + 8) == -5             # misaligned workspace
 
 
+def test_paged_prefill_form():
+    form = attn.attn_fwd_paged_form
+    # the paper's paged prefill: 7 blocks x 24 heads = 168 workgroups
+    assert form(1, 892, 892, 24, True) == attn.ATTN_FWD_PAGED_KEY_HALVES
+    assert form(1, 892, 892, 24, False) == attn.ATTN_FWD_PAGED_KEY_HALVES
+    # 5 x 24 = 120 workgroups: split when a workspace is given
+    assert form(1, 640, 892, 24, True) == attn.ATTN_FWD_PAGED_SPLIT
+    assert form(1, 640, 892, 24, False) == attn.ATTN_FWD_PAGED_KEY_HALVES
+    assert form(1, 640, 256, 24, True) == attn.ATTN_FWD_PAGED_KEY_HALVES   # one chunk
+    assert form(64, 4096, 4096, 32, True) == attn.ATTN_FWD_PAGED_UNSPLIT
+    assert form(2, 128, 600, 128, False) == attn.ATTN_FWD_PAGED_UNSPLIT      # exactly 256
+    assert form(1, 128, 600, 255, False) == attn.ATTN_FWD_PAGED_KEY_HALVES   # 255
+    # the workspace size agrees: non-zero exactly when the form is the split
+    for args in [(1, 892, 892, 24), (1, 640, 892, 24), (2, 150, 600, 4), (64, 4096, 4096, 32)]:
+        b, mq, mk, hq = args
+        split = form(b, mq, mk, hq, True) == attn.ATTN_FWD_PAGED_SPLIT
+        assert (attn.attn_fwd_paged_workspace_size(b, mq, b * mq, mk, hq, 1, 128) > 0) == split
+    for bad in [(0, 892, 892, 24, True), (1, 0, 892, 24, True), (1, 892, -1, 24, True),
+                (1, 892, 892, 0, True)]:
+        assert attn.lib().attn_fwd_paged_form(*[int(v) for v in bad]) == -2
+    assert attn.lib().attn_fwd_paged_form(1, 892, 892, 24, 2) == -8
+
+
 def test_paged_prefill_workspace_size():
     size = attn.attn_fwd_paged_workspace_size
     # split: 2 x 4 x 1 unsplit workgroups, 600 keys -> 3 chunks of 256

@@ -61,7 +61,14 @@ def _check(o, lse, ro, rl, label):
     assert el <= LSE_MAXABS, (label, el)
 
 
-def _prefill(q, kc, vc, qo, kv, idx, causal, scale, label, split=True):
+def _prefill(q, kc, vc, qo, kv, idx, causal, scale, label, split=True, form=None):
+    """Paged prefill against the oracle; `form`, when given, is the form
+    (attn.ATTN_FWD_PAGED_*) the library must report for these shapes."""
+    if form is not None:
+        got = attn.attn_fwd_paged_form(len(qo) - 1, max(b - a for a, b in zip(qo, qo[1:])),
+                                       max(b - a for a, b in zip(kv, kv[1:])), q.shape[1],
+                                       split)
+        assert got == form, (label, got, form)
     dq, dkc, dvc = _dev(q, kc, vc)
     o, lse = attn.forward_paged(dq, dkc, dvc, _i32(qo), _i32(kv), _i32(idx),
                                 max(b - a for a, b in zip(qo, qo[1:])), causal, scale,
@@ -84,9 +91,12 @@ def test_paged_prefill(D, causal, Hq, Hkv, split):
     q_lens = [200, 37, 1, 70, 0, 129, 700, 600]
     kv_lens = [200, 300, 1, 5, 0, 129, 900, 520]
     args = _draw(1, q_lens, kv_lens, Hq, Hkv, D, 4000)
-    announce(f"paged prefill D={D} causal={causal} Hq={Hq} Hkv={Hkv} split={split}")
+    # 8 requests x Hq heads x 6 blocks of 128 queries: 96, 192 or 288 workgroups
+    form = {2: attn.ATTN_FWD_PAGED_SPLIT if split else attn.ATTN_FWD_PAGED_KEY_HALVES,
+            4: attn.ATTN_FWD_PAGED_KEY_HALVES, 6: attn.ATTN_FWD_PAGED_UNSPLIT}[Hq]
+    announce(f"paged prefill D={D} causal={causal} Hq={Hq} Hkv={Hkv} split={split} form={form}")
     _prefill(*args, causal, D ** -0.5, f"prefill d{D} c{int(causal)} g{Hq // Hkv} s{int(split)}",
-             split)
+             split, form)
 
 
 def _decode(q, kc, vc, kv, idx, max_kvlen, scale, label):
@@ -190,4 +200,4 @@ def test_full_paged_workload(name):
     else:
         for split in (True, False):
             _prefill(x.q, x.k_cache, x.v_cache, x.qo_indptr, x.kv_indptr, x.kv_indices, w.causal,
-                     w.scale, f"{name} split={split}", split)
+                     w.scale, f"{name} split={split}", split, attn.ATTN_FWD_PAGED_KEY_HALVES)

@@ -55,6 +55,14 @@ def test_shapes_gqa(Hq, Hkv, D, causal):
     _fixed_case(190, D, causal, Hq=Hq, Hkv=Hkv, B=2)
 
 
+def test_workgroup_order_short_last_window():
+    """17 key/value head groups (not a multiple of the 8 XCDs) of 16 query
+    heads and 8 causal blocks of 128 queries: the forward's and dQ's
+    workgroup order then takes windows of two groups per XCD, the last one
+    short, and leaves unused slots on some XCDs."""
+    _fixed_case(1024, 64, True, Hq=16, Hkv=1, B=17)
+
+
 @pytest.mark.parametrize("D", [64, 96, 128])
 def test_long_ragged_sequence(D):
     _fixed_case(1000, D, True, Hq=2, Hkv=1)

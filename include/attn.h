@@ -83,15 +83,16 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
              int B, int Hq, int Hkv, int S, int D, int causal, float scale,
              hipStream_t stream);
 
-/* Bytes of backward workspace for the fixed-length layout (fp32 Delta and
+/* Bytes of backward workspace for the fixed-length layout (fp32 -Delta and
  * fp32 L log2(e), one of each per query row and head). */
 size_t attn_bwd_workspace_size(int B, int Hq, int Hkv, int S, int D);
 
 /*
  * Backward, fixed length.  Consumes q, k, v, the forward's o and lse, and
  * dO; writes dq [B,Hq,S,D] and dk, dv [B,Hkv,S,D] (dk, dv summed over each
- * query-head group).  Delta_i = sum_d dO_id * O_id and lse_i * log2(e) are
- * precomputed into the workspace; P is recomputed from them.  The gradients are of the loss
+ * query-head group).  Delta_i = sum_d dO_id * O_id (stored negated) and
+ * lse_i * log2(e) are precomputed into the workspace; P is recomputed from
+ * them.  The gradients are of the loss
  * sum(dO * O) with O = attention(q, k, v).  The result is deterministic
  * (no atomics).
  */
@@ -104,7 +105,7 @@ int attn_bwd(const void* q, const void* k, const void* v, const void* o,
  * Backward, fixed length, for callers that cannot allocate memory (code
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc): attn_bwd without a workspace argument.  Its scratch (the
- * same fp32 Delta and L log2(e) arrays) is a device array inside the
+ * same fp32 -Delta and L log2(e) arrays) is a device array inside the
  * library of ATTN_BWD_NOALLOC_SCRATCH_BYTES, which every GPU the library
  * runs on holds until the process ends; the call itself allocates nothing.
  * A problem whose attn_bwd_workspace_size exceeds it (B * Hq * S above
@@ -132,7 +133,7 @@ int attn_fwd_varlen(const void* q, const void* k, const void* v, void* o,
                     int max_seqlen, int total, int Hq, int Hkv, int D,
                     int causal, float scale, hipStream_t stream);
 
-/* Bytes of backward workspace for the packed layout (fp32 Delta and fp32
+/* Bytes of backward workspace for the packed layout (fp32 -Delta and fp32
  * L log2(e), one of each per query row and head). */
 size_t attn_bwd_varlen_workspace_size(int total, int Hq, int Hkv, int D);
 
@@ -147,7 +148,7 @@ int attn_bwd_varlen(const void* q, const void* k, const void* v,
 /*
  * The backward in separately enqueued phases, for callers that time or
  * schedule its two kernels on their own.  `phases` is a bit mask:
- *   ATTN_BWD_DQ   computes Delta and lse * log2(e) into the workspace,
+ *   ATTN_BWD_DQ   computes -Delta and lse * log2(e) into the workspace,
  *                 then dq;
  *   ATTN_BWD_DKDV computes dk and dv from the workspace of an ATTN_BWD_DQ phase
  *                 enqueued earlier on the same stream with the same

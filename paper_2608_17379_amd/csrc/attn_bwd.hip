@@ -11,8 +11,8 @@
 //  * bwd_dq_kernel: one workgroup of 4 wavefronts per (segment, query head,
 //    128-row query block; the blocks with the most key tiles first), 32 rows
 //    per wavefront, two workgroups per CU.  Its prologue computes Delta for its rows (the rows'
-//    dO and O are read once) and stores it, with L log2(e), in the
-//    workspace; the loop over key tiles recomputes S^T = K Q^T and
+//    dO and O are read once) and stores -Delta, with L log2(e), in the
+//    workspace (the dK/dV kernels start their dP accumulators from -Delta); the loop over key tiles recomputes S^T = K Q^T and
 //    dP^T = V dO^T, forms dS^T in registers and accumulates dQ^T += K^T dS^T.
 //  * bwd_dkdv_kernel / bwd_dkdv4_kernel: one workgroup per (segment,
 //    key/value head, 128 keys), launched after bwd_dq_kernel (they read the
@@ -25,7 +25,7 @@
 //    rounds of it use bwd_dkdv_kernel, with 8 wavefronts and one workgroup
 //    per CU (see dkdv_form_for).
 //
-// Tiles of 64 rows (K and V for dQ; Q, dO, L log2 e and Delta for dK/dV, in
+// Tiles of 64 rows (K and V for dQ; Q, dO, L log2 e and -Delta for dK/dV, in
 // 32-row steps for bwd_dkdv4_kernel) go from global memory straight into a
 // ring of LDS stages (buffer_load ... lds,
 // bounded at the segment end so that rows past it read as zero), issued a
@@ -157,7 +157,7 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
     }
     const float delta = sum_halves(dsum);
     if (valid && half == 0) {
-      a.delta[roff + qrow] = delta;
+      a.delta[roff + qrow] = -delta;   // negated: the dK/dV kernels start dP from it
       a.lse2[roff + qrow] = lse2;
     }
 
@@ -419,12 +419,18 @@ __global__ __launch_bounds__(64 * kDkvWaves, 1) void bwd_dkdv_kernel(BwdArgs a) 
     const float* lse = reinterpret_cast<const float*>(smem + SM::LSE + st * 256);
     const float* del = reinterpret_cast<const float*>(smem + SM::DEL + st * 256);
     const int qs0 = (it0 + per_head - 1 - n % per_head) * kTileRows + 32 * hq;
-    // S = Q K^T, dP = dO V^T for this wavefront's 32 queries x 32 keys.
+    // S = Q K^T, dP - Delta = dO V^T - Delta for this wavefront's 32 queries
+    // x 32 keys: dP starts from the workspace's -Delta of each element's
+    // query (s[r], dp[r]: query qs0 + 8(r/4) + 4half + r%4, key krow).
     f32x16 s, dp;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      s[r] = 0.f;
-      dp[r] = 0.f;
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 nd4 = *reinterpret_cast<const f32x4*>(&del[32 * hq + 8 * g + 4 * half]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        s[4 * g + i] = 0.f;
+        dp[4 * g + i] = nd4[i];
+      }
     }
 #pragma unroll
     for (int c = 0; c < D / 16; ++c) {
@@ -432,19 +438,17 @@ __global__ __launch_bounds__(64 * kDkvWaves, 1) void bwd_dkdv_kernel(BwdArgs a) 
       s = mfma32(ld16(q + o), ld16(krd + rr.rm[c]), s);
       dp = mfma32(ld16(dout + o), ld16(vrd + rr.rm[c]), dp);
     }
-    // s[r], dp[r]: query qs0 + 8(r/4) + 4half + r%4, key krow.
     const int t = krow - qs0 - 4 * half;   // key minus the lane's first query
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse[32 * hq + 8 * g + 4 * half]);
-      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&del[32 * hq + 8 * g + 4 * half]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = 4 * g + i;
         float p = fast_exp2(__builtin_fmaf(s[r], sl2, -l4[i]));
         if constexpr (decltype(masked)::value) p = t > 8 * g + i ? 0.f : p;   // key after query
         s[r] = p;
-        dp[r] = p * (dp[r] - d4[i]);
+        dp[r] = p * dp[r];
       }
     }
     // dV^T[d][key] += sum_q dO^T[d][q] P[q][key];  dK^T += Q^T dS, with the
@@ -681,11 +685,18 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
     const float* lse = reinterpret_cast<const float*>(smem + SM::LSE + st * (kQS * 4));
     const float* del = reinterpret_cast<const float*>(smem + SM::DEL + st * (kQS * 4));
     const int qs0 = (it0 + per_head - 1 - n % per_head) * kQS;
+    // S = Q K^T and dP - Delta = dO V^T - Delta: dP starts from the
+    // workspace's -Delta of each element's query (s[r], dp[r]: query
+    // qs0 + 8(r/4) + 4half + r%4, key krow).
     f32x16 s, dp;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      s[r] = 0.f;
-      dp[r] = 0.f;
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 nd4 = *reinterpret_cast<const f32x4*>(&del[8 * g + 4 * half]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        s[4 * g + i] = 0.f;
+        dp[4 * g + i] = nd4[i];
+      }
     }
 #pragma unroll
     for (int c = 0; c < D / 16; ++c) {
@@ -694,19 +705,17 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
       // Keep at most four chunks of operands in flight (register budget).
       if (c % 4 == 3) __builtin_amdgcn_sched_barrier(0);
     }
-    // s[r], dp[r]: query qs0 + 8(r/4) + 4half + r%4, key krow.
     const int t = krow - qs0 - 4 * half;   // key minus the lane's first query
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse[8 * g + 4 * half]);
-      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&del[8 * g + 4 * half]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = 4 * g + i;
         float p = fast_exp2(__builtin_fmaf(s[r], sl2, -l4[i]));
         if constexpr (decltype(masked)::value) p = t > 8 * g + i ? 0.f : p;   // key after query
         s[r] = p;
-        dp[r] = p * (dp[r] - d4[i]);
+        dp[r] = p * dp[r];
       }
     }
     // dV^T += dO^T P, dK^T += Q^T dS (A operands read transposed).

@@ -47,6 +47,67 @@ namespace {
 
 constexpr int kTileRows = 64;
 
+// The query-side rows that a dK/dV workgroup copies, pair by pair of its
+// loop: pair n is query head g = n / per_head of the group and step
+// j = n % per_head, whose rows start at (it0 + per_head - 1 - j) ROWS (the
+// steps of a head are walked from the last down).  The walk holds j and the
+// current head's row-0 pointers and moves them by addition, so the loop
+// needs no division and no 64-bit products.  A row of a q-like tensor is
+// below 2^24 bytes (128 rows are below 2^31, which the API checks), so row
+// offsets are 32-bit products, and each descriptor covers the rows from its
+// step to the segment end (row0 < len always), capped at whole rows below
+// 2^31 bytes.
+template <int ROWS>
+struct QueryWalk {
+  const char* q;      // the current head's row 0 (segment start)
+  const char* dout;
+  const char* lse;
+  const char* del;
+  int64_t q_head_b, r_head_b;   // bytes from one query head to the next
+  int row_b, cap_rows, len, top, per_head;
+  int j = 0;
+  static constexpr int kCap4 = 0x7fffffff / 4;
+  __device__ __forceinline__ int row0() const { return top - j * ROWS; }
+  __device__ __forceinline__ i32x4 q_desc() const {
+    return rows_desc_rb(q, row0(), len, row_b, cap_rows);
+  }
+  __device__ __forceinline__ i32x4 dout_desc() const {
+    return rows_desc_rb(dout, row0(), len, row_b, cap_rows);
+  }
+  __device__ __forceinline__ i32x4 lse_desc() const { return rows_desc_rb(lse, row0(), len, 4, kCap4); }
+  __device__ __forceinline__ i32x4 del_desc() const { return rows_desc_rb(del, row0(), len, 4, kCap4); }
+  __device__ __forceinline__ void next() {
+    if (++j == per_head) {
+      j = 0;
+      q += q_head_b;
+      dout += q_head_b;
+      lse += r_head_b;
+      del += r_head_b;
+    }
+  }
+};
+
+template <int ROWS>
+__device__ __forceinline__ QueryWalk<ROWS> query_walk(const BwdArgs& a, int64_t qseg,
+                                                      int64_t rseg, int hk, int len, int it0,
+                                                      int per_head) {
+  QueryWalk<ROWS> w;
+  const Layout& L = a.L;
+  const int64_t h0 = (int64_t)hk * L.group;
+  w.q = reinterpret_cast<const char*>(a.q + qseg + h0 * L.q_head);
+  w.dout = reinterpret_cast<const char*>(a.dout + qseg + h0 * L.q_head);
+  w.lse = reinterpret_cast<const char*>(a.lse2 + rseg + h0 * L.r_head);
+  w.del = reinterpret_cast<const char*>(a.delta + rseg + h0 * L.r_head);
+  w.q_head_b = L.q_head * 2;
+  w.r_head_b = L.r_head * 4;
+  w.row_b = (int)(L.q_row * 2);
+  w.cap_rows = 0x7fffffff / w.row_b;
+  w.len = len;
+  w.top = (it0 + per_head - 1) * ROWS;
+  w.per_head = per_head;
+  return w;
+}
+
 // ---------------------------------------------------------------------------
 // dQ (and Delta)
 //
@@ -98,10 +159,11 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
   const int len = seg.len;
   const float sl2 = a.scale_log2;
   const float scale = a.scale;
-  const int64_t kv_row_b = L.kv_row * 2;
+  const int kv_rb = (int)(L.kv_row * 2);   // below 2^24: k-like rows are no wider than q-like
+  const int kv_cap = 0x7fffffff / kv_rb;
   const int64_t q_row = L.q_row;
   const uint32_t sbase = lds_addr(smem);
-  const Tile dma(wave, lane, (int)kv_row_b);
+  const Tile dma(wave, lane, kv_rb);
   const RowReader<D> rr(l32, half);
   const TransReader<D> trr(lane);
 
@@ -113,8 +175,8 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
     const int64_t kvoff = (int64_t)seg.start * L.kv_row + (int64_t)z * L.kv_batch +
                           (int64_t)hk * L.kv_head;
     const int64_t roff = (int64_t)seg.start + (int64_t)z * L.r_batch + (int64_t)h * L.r_head;
-    const uint16_t* const kp = a.k + kvoff;
-    const uint16_t* const vp = a.v + kvoff;
+    const char* const kp = reinterpret_cast<const char*>(a.k + kvoff);
+    const char* const vp = reinterpret_cast<const char*>(a.v + kvoff);
 
     const int qw0 = q0 + wave * 32;
     const int qrow = qw0 + l32;
@@ -124,8 +186,11 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
     const int nkt = (kend + kTileRows - 1) / kTileRows;
     auto issue = [&](int kt) __attribute__((always_inline)) {
       const uint32_t st = (uint32_t)(kt & 1) * SM::TILE;
-      dma_tile<D>(dma, rows_desc(kp, kt * kTileRows, len, kv_row_b), sbase + SM::K + st, wave);
-      dma_tile<D>(dma, rows_desc(vp, kt * kTileRows, len, kv_row_b), sbase + SM::V + st, wave);
+      // kt < nkt, so the tile starts before the segment end.
+      dma_tile<D>(dma, rows_desc_rb(kp, kt * kTileRows, len, kv_rb, kv_cap), sbase + SM::K + st,
+                  wave);
+      dma_tile<D>(dma, rows_desc_rb(vp, kt * kTileRows, len, kv_rb, kv_cap), sbase + SM::V + st,
+                  wave);
     };
     // Both stages are free: the first two tiles go out before the row loads.
     issue(0);
@@ -347,13 +412,7 @@ __global__ __launch_bounds__(64 * kDkvWaves, 1) void bwd_dkdv_kernel(BwdArgs a) 
   const int krow = kw0 + l32;
   // Fields used inside the lambdas below, as plain values (capturing the
   // kernel argument itself would make the compiler spill it to scratch).
-  const uint16_t* const qbase = a.q;
-  const uint16_t* const dobase = a.dout;
-  const float* const lsebase = a.lse2;   // lse * log2(e), written by the dQ kernel
-  const float* const delbase = a.delta;
   const int group = L.group;
-  const int64_t q_head = L.q_head, r_head = L.r_head;
-  const int64_t q_row_b = L.q_row * 2;
   const int len = seg.len;
   const float sl2 = a.scale_log2;
 
@@ -363,8 +422,11 @@ __global__ __launch_bounds__(64 * kDkvWaves, 1) void bwd_dkdv_kernel(BwdArgs a) 
   const int nqt = (seg.len + kTileRows - 1) / kTileRows;
   const int per_head = nqt - it0;
   const int niter = per_head * L.group;
+  const int top = (it0 + per_head - 1) * kTileRows;   // first row of each head's first tile
+  // Q, dO, L log2(e) (written by the dQ kernel) and -Delta rows of the tiles.
+  QueryWalk<kTileRows> walk = query_walk<kTileRows>(a, qseg, rseg, hk, len, it0, per_head);
 
-  const Tile qdma(wave, lane, (int)q_row_b);
+  const Tile qdma(wave, lane, (int)(L.q_row * 2));
   const RowReader<D> rr(l32, half);
   const TransReader<D> trr(lane);
   const uint32_t sbase = lds_addr(smem);
@@ -382,20 +444,15 @@ __global__ __launch_bounds__(64 * kDkvWaves, 1) void bwd_dkdv_kernel(BwdArgs a) 
     }
   }
 
-  auto issue = [&](int n, int st) __attribute__((always_inline)) {
-    const int g = n / per_head;
-    const int qb = (it0 + per_head - 1 - n % per_head) * kTileRows;
-    const int h = hk * group + g;
-    const int64_t qoff = qseg + (int64_t)h * q_head;
-    dma_tile<D>(qdma, rows_desc(qbase + qoff, qb, len, q_row_b), sbase + SM::Q + st * SM::TILE,
-                wave);
-    dma_tile<D>(qdma, rows_desc(dobase + qoff, qb, len, q_row_b), sbase + SM::DO + st * SM::TILE,
-                wave);
+  // Copies of the walk's next tile into stage st.
+  auto issue = [&](int st) __attribute__((always_inline)) {
+    dma_tile<D>(qdma, walk.q_desc(), sbase + SM::Q + st * SM::TILE, wave);
+    dma_tile<D>(qdma, walk.dout_desc(), sbase + SM::DO + st * SM::TILE, wave);
     if (wave == 0 && lane < 16) {
-      const int64_t r = rseg + (int64_t)h * r_head;
-      dma16(rows_desc(lsebase + r, qb, len, 4), sbase + SM::LSE + st * 256, 16 * lane);
-      dma16(rows_desc(delbase + r, qb, len, 4), sbase + SM::DEL + st * 256, 16 * lane);
+      dma16(walk.lse_desc(), sbase + SM::LSE + st * 256, 16 * lane);
+      dma16(walk.del_desc(), sbase + SM::DEL + st * 256, 16 * lane);
     }
+    walk.next();
   };
 
   f32x16 dkacc[D / 32], dvacc[D / 32];
@@ -411,14 +468,14 @@ __global__ __launch_bounds__(64 * kDkvWaves, 1) void bwd_dkdv_kernel(BwdArgs a) 
   const uint16_t* const krd = sk + (kq >> 1) * (SM::TILE / 2) + 32 * (kq & 1) * P;
   const uint16_t* const vrd = sv + (kq >> 1) * (SM::TILE / 2) + 32 * (kq & 1) * P;
 
-  // Query half hq (32 queries) of tile n, in stage st, against this
-  // wavefront's 32 keys.
-  auto compute = [&](int n, int st, int hq, auto masked) __attribute__((always_inline)) {
+  // Query half hq (32 queries) of the tile whose first row is qt0, in stage
+  // st, against this wavefront's 32 keys.
+  auto compute = [&](int qt0, int st, int hq, auto masked) __attribute__((always_inline)) {
     const uint16_t* q = reinterpret_cast<const uint16_t*>(smem + SM::Q + st * SM::TILE);
     const uint16_t* dout = reinterpret_cast<const uint16_t*>(smem + SM::DO + st * SM::TILE);
     const float* lse = reinterpret_cast<const float*>(smem + SM::LSE + st * 256);
     const float* del = reinterpret_cast<const float*>(smem + SM::DEL + st * 256);
-    const int qs0 = (it0 + per_head - 1 - n % per_head) * kTileRows + 32 * hq;
+    const int qs0 = qt0 + 32 * hq;
     // S = Q K^T, dP - Delta = dO V^T - Delta for this wavefront's 32 queries
     // x 32 keys: dP starts from the workspace's -Delta of each element's
     // query (s[r], dp[r]: query qs0 + 8(r/4) + 4half + r%4, key krow).
@@ -474,23 +531,26 @@ __global__ __launch_bounds__(64 * kDkvWaves, 1) void bwd_dkdv_kernel(BwdArgs a) 
   // of each head (those reaching below the causal diagonal of this
   // workgroup's keys) are masked; rows past the end need no mask, as their
   // Q and dO read as zero.
-  auto step = [&](int n, auto masked) __attribute__((always_inline)) {
+  // Step n, the tile of head n / per_head whose first row is qt0.
+  auto step = [&](int n, int qt0, auto masked) __attribute__((always_inline)) {
     wait_vm_all();
     __syncthreads();
-    if (n + 1 < niter) issue(n + 1, (n + 1) & 1);
-    compute(n, n & 1, sb, masked);
+    if (n + 1 < niter) issue((n + 1) & 1);
+    compute(qt0, n & 1, sb, masked);
   };
   // Each head's query tiles are walked from the last down to the diagonal,
   // so that the workgroups of one key/value head (all starting with the
   // head's last tiles) read the same Q and dO tiles at about the same time
   // and share them in their XCD's L2; the two masked tiles come last.
   const int nmask = CAUSAL ? min(2, per_head) : 0;
-  issue(0, 0);
+  issue(0);
   int n = 0;
   for (int g = 0; g < group; ++g) {
     const int nend = n + per_head;
-    for (const int nu = nend - nmask; n < nu; ++n) step(n, std::false_type{});
-    for (; n < nend; ++n) step(n, std::true_type{});
+    int qt0 = top;
+    for (const int nu = nend - nmask; n < nu; ++n, qt0 -= kTileRows)
+      step(n, qt0, std::false_type{});
+    for (; n < nend; ++n, qt0 -= kTileRows) step(n, qt0, std::true_type{});
   }
 
   // Epilogue.  Rows are staged as bf16 in LDS ([32 keys][D], 16-byte chunks
@@ -611,13 +671,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
   const int64_t rseg = (int64_t)seg.start + (int64_t)z * L.r_batch;
   const int kw0 = k0 + 32 * kq;
   const int krow = kw0 + l32;
-  const uint16_t* const qbase = a.q;
-  const uint16_t* const dobase = a.dout;
-  const float* const lsebase = a.lse2;
-  const float* const delbase = a.delta;
   const int group = L.group;
-  const int64_t q_head = L.q_head, r_head = L.r_head;
-  const int64_t q_row_b = L.q_row * 2;
   const int len = seg.len;
   const float sl2 = a.scale_log2;
 
@@ -627,8 +681,10 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
   const int nqs = (seg.len + kQS - 1) / kQS;
   const int per_head = nqs - it0;
   const int niter = per_head * L.group;
+  const int top = (it0 + per_head - 1) * kQS;   // first row of each head's first step
+  QueryWalk<kQS> walk = query_walk<kQS>(a, qseg, rseg, hk, len, it0, per_head);
 
-  const HTile qdma(wave, lane, (int)q_row_b);
+  const HTile qdma(wave, lane, (int)(L.q_row * 2));
   const RowReader<D> rr(l32, half);
   const TransReader<D> trr(lane);
   const uint32_t sbase = lds_addr(smem);
@@ -651,20 +707,15 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
     for (int c = 0; c < D / 16; ++c) kreg[c] = bload16(rk, base + 32 * c);
   }
 
-  auto issue = [&](int n, int st) __attribute__((always_inline)) {
-    const int g = n / per_head;
-    const int qb = (it0 + per_head - 1 - n % per_head) * kQS;
-    const int h = hk * group + g;
-    const int64_t qoff = qseg + (int64_t)h * q_head;
-    dma_tile<D>(qdma, rows_desc(qbase + qoff, qb, len, q_row_b), sbase + SM::Q + st * SM::HT,
-                wave);
-    dma_tile<D>(qdma, rows_desc(dobase + qoff, qb, len, q_row_b), sbase + SM::DO + st * SM::HT,
-                wave);
+  // Copies of the walk's next step into stage st.
+  auto issue = [&](int st) __attribute__((always_inline)) {
+    dma_tile<D>(qdma, walk.q_desc(), sbase + SM::Q + st * SM::HT, wave);
+    dma_tile<D>(qdma, walk.dout_desc(), sbase + SM::DO + st * SM::HT, wave);
     if (wave == 0 && lane < 8) {
-      const int64_t r = rseg + (int64_t)h * r_head;
-      dma16(rows_desc(lsebase + r, qb, len, 4), sbase + SM::LSE + st * (kQS * 4), 16 * lane);
-      dma16(rows_desc(delbase + r, qb, len, 4), sbase + SM::DEL + st * (kQS * 4), 16 * lane);
+      dma16(walk.lse_desc(), sbase + SM::LSE + st * (kQS * 4), 16 * lane);
+      dma16(walk.del_desc(), sbase + SM::DEL + st * (kQS * 4), 16 * lane);
     }
+    walk.next();
   };
 
   f32x16 dkacc[D / 32], dvacc[D / 32];
@@ -678,13 +729,12 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
   // This wavefront's V rows: tile kq / 2, rows 32 (kq % 2) + l32.
   const uint16_t* const vrd = sv + (kq >> 1) * (SM::TILE / 2) + 32 * (kq & 1) * P;
 
-  // The 32 queries of step n (stage st) against this wavefront's 32 keys.
-  auto compute = [&](int n, int st, auto masked) __attribute__((always_inline)) {
+  // The 32 queries from qs0 (stage st) against this wavefront's 32 keys.
+  auto compute = [&](int qs0, int st, auto masked) __attribute__((always_inline)) {
     const uint16_t* q = reinterpret_cast<const uint16_t*>(smem + SM::Q + st * SM::HT);
     const uint16_t* dout = reinterpret_cast<const uint16_t*>(smem + SM::DO + st * SM::HT);
     const float* lse = reinterpret_cast<const float*>(smem + SM::LSE + st * (kQS * 4));
     const float* del = reinterpret_cast<const float*>(smem + SM::DEL + st * (kQS * 4));
-    const int qs0 = (it0 + per_head - 1 - n % per_head) * kQS;
     // S = Q K^T and dP - Delta = dO V^T - Delta: dP starts from the
     // workspace's -Delta of each element's query (s[r], dp[r]: query
     // qs0 + 8(r/4) + 4half + r%4, key krow).
@@ -743,7 +793,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
   auto sync = [&](int n) __attribute__((always_inline)) {
     wait_vm_all();
     __syncthreads();
-    if (n + 1 < niter) issue(n + 1, (n + 1) & 1);
+    if (n + 1 < niter) issue((n + 1) & 1);
   };
   // Per head the query steps are walked from the last down to the
   // diagonal, so that the workgroups of one key/value head (all starting
@@ -754,7 +804,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
   // need no mask.  Each loop body has one form of compute (two forms in one
   // body exceed the register budget).
   const int ndiag = CAUSAL ? min(kKN / kQS, per_head) : 0;
-  issue(0, 0);
+  issue(0);
   // Wait for every load so far (K rows, V tile, step 0) through the builtin,
   // which the compiler's wait insertion sees (the first step waits for them
   // anyway).  Without it the compiler takes the K-row loads as possibly
@@ -764,15 +814,16 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv4_kernel(BwdArgs a) {
   int n = 0;
 #pragma nounroll
   for (int g = 0; g < group; ++g) {
+    int qs0 = top;   // first query of step n
 #pragma nounroll
-    for (const int nu = (g + 1) * per_head - ndiag; n < nu; ++n) {
+    for (const int nu = (g + 1) * per_head - ndiag; n < nu; ++n, qs0 -= kQS) {
       sync(n);
-      compute(n, n & 1, std::false_type{});
+      compute(qs0, n & 1, std::false_type{});
     }
 #pragma nounroll
-    for (const int ne = (g + 1) * per_head; n < ne; ++n) {
+    for (const int ne = (g + 1) * per_head; n < ne; ++n, qs0 -= kQS) {
       sync(n);
-      if ((it0 + per_head - 1 - n % per_head) * kQS >= kw0) compute(n, n & 1, std::true_type{});
+      if (qs0 >= kw0) compute(qs0, n & 1, std::true_type{});
     }
   }
 

@@ -150,7 +150,10 @@ __global__ __launch_bounds__(kThreads * KS, KS == 1 ? 2 : 1) void fwd_kernel(Fwd
     // Fields used inside the lambdas below, as plain values (capturing the
     // kernel argument itself can make the compiler spill it to scratch).
     const bool causal = a.causal != 0;
-    const int64_t kv_row = L.kv_row;
+    // K/V rows are below 2^24 bytes (no wider than a q-like row, and 128
+    // q-like rows are below 2^31 bytes, which the API checks).
+    const int kv_rb = (int)(L.kv_row * 2);
+    const int kv_cap = 0x7fffffff / kv_rb;
 
     // Paged keys: tile rows are gathered through the page indices, which are
     // fetched one tile ahead of the copies that use them.
@@ -182,8 +185,11 @@ __global__ __launch_bounds__(kThreads * KS, KS == 1 ? 2 : 1) void fwd_kernel(Fwd
         dma.load_at(vcache, off, vd, wave);
         if (kt + KS < kt_hi) fetch(kt + KS);
       } else {
-        dma.load(rows_rsrc(kp, kt * kBN, kv_len, kv_row), kd, wave);
-        dma.load(rows_rsrc(vp, kt * kBN, kv_len, kv_row), vd, wave);
+        // kt < nkt, so the tile starts before kv_len.
+        dma.load(rows_rsrc_rb(reinterpret_cast<const char*>(kp), kt * kBN, kv_len, kv_rb, kv_cap),
+                 kd, wave);
+        dma.load(rows_rsrc_rb(reinterpret_cast<const char*>(vp), kt * kBN, kv_len, kv_rb, kv_cap),
+                 vd, wave);
       }
     };
 

@@ -279,19 +279,47 @@ __device__ __forceinline__ i32x4 rows_desc(const void* head_base, int row0, int 
                    (int64_t)(len - row0) * row_stride_bytes);
 }
 
+// A raw buffer descriptor over `bytes` bytes at `base`; bytes in [0, 2^31).
+__device__ __forceinline__ i32x4 raw_desc(const char* base, int bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  return i32x4{(int)(uint32_t)a, (int)((uint32_t)(a >> 32) & 0xffffu), bytes, kRsrcFlags};
+}
+
+// Rows [row0, len) of a tensor whose rows are rb bytes apart, from `base`
+// (its row 0), with 0 <= row0 < len and rb < 2^24: 32-bit products only,
+// the range capped at cap_rows = (2^31 - 1) / rb whole rows.
+__device__ __forceinline__ i32x4 rows_desc_rb(const char* base, int row0, int len, int rb,
+                                              int cap_rows) {
+  return raw_desc(base + (int64_t)row0 * rb, min(len - row0, cap_rows) * rb);
+}
+
+// The same rows as a buffer resource for the compiler's buffer builtins.
+__device__ __forceinline__ rsrc_t rows_rsrc_rb(const char* base, int row0, int len, int rb,
+                                               int cap_rows) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base) + (int64_t)row0 * rb, (short)0,
+                                           min(len - row0, cap_rows) * rb, kRsrcFlags);
+}
+
 // LDS byte address of a __shared__ object.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(ATTN_LDS const void*)p;
 }
 
-// One 16-byte-per-lane DMA: lane L's 16 bytes at byte voff of the buffer go
-// to LDS byte lds_base + 16 L.  M0 is saved and restored around the load.
+// 16-byte-per-lane DMAs written as inline assembly, so that the compiler's
+// wait insertion does not count them (the kernels wait for them explicitly).
+// The LDS destination of buffer_load ... lds comes from M0; on the gfx9
+// family an LDS DMA needs one wait state after an SALU write of M0, hence
+// the s_nop after each write.  M0 is saved and restored around each block.
+//
+// One DMA: lane L's 16 bytes at byte voff of the buffer go to LDS byte
+// lds_base + 16 L.
 __device__ __forceinline__ void dma16(i32x4 desc, uint32_t lds_base, int voff) {
   uint32_t saved;
   lds_base = __builtin_amdgcn_readfirstlane(lds_base);
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
       "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
       "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
@@ -299,12 +327,60 @@ __device__ __forceinline__ void dma16(i32x4 desc, uint32_t lds_base, int voff) {
       : "memory");
 }
 
+// NJ DMAs in one block (NJ = 1, 2 or 4): DMA j takes byte voff[j] of the
+// buffer to LDS byte lds_base + 1024 j + 16 L; M0 is set once and stepped
+// by 1 KiB.
+template <int NJ>
+__device__ __forceinline__ void dma16_n(i32x4 desc, uint32_t lds_base, const int (&voff)[NJ]) {
+  if constexpr (NJ == 1) {
+    dma16(desc, lds_base, voff[0]);
+  } else if constexpr (NJ == 2) {
+    uint32_t saved;
+    lds_base = __builtin_amdgcn_readfirstlane(lds_base);
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %2, %4, 0 offen lds\n\t"
+        "s_add_u32 m0, m0, 0x400\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %3, %4, 0 offen lds\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds_base), "v"(voff[0]), "v"(voff[1]), "s"(desc)
+        : "memory", "scc");
+  } else {
+    static_assert(NJ == 4, "1, 2 or 4 DMAs per block");
+    uint32_t saved;
+    lds_base = __builtin_amdgcn_readfirstlane(lds_base);
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %2, %6, 0 offen lds\n\t"
+        "s_add_u32 m0, m0, 0x400\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %3, %6, 0 offen lds\n\t"
+        "s_add_u32 m0, m0, 0x400\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %4, %6, 0 offen lds\n\t"
+        "s_add_u32 m0, m0, 0x400\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %5, %6, 0 offen lds\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds_base), "v"(voff[0]), "v"(voff[1]), "v"(voff[2]), "v"(voff[3]), "s"(desc)
+        : "memory", "scc");
+  }
+}
+
+// This wavefront's share of a tile (instructions wave NJ .. wave NJ + NJ - 1
+// of the tile's copy, 1 KiB of LDS each).
 template <int D, int NW>
 __device__ __forceinline__ void dma_tile(const AsyncTile<D, NW>& t, i32x4 desc, uint32_t tile_base,
                                          int wave) {
-#pragma unroll
-  for (int j = 0; j < AsyncTile<D, NW>::NJ; ++j)
-    dma16(desc, tile_base + (uint32_t)((wave * AsyncTile<D, NW>::NJ + j) * 64 * 16), t.goff[j]);
+  constexpr int NJ = AsyncTile<D, NW>::NJ;
+  dma16_n<NJ>(desc, tile_base + (uint32_t)(wave * NJ * 64 * 16), t.goff);
 }
 
 // Wait for this wavefront's vector-memory operations, including the DMAs

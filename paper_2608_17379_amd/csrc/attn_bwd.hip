@@ -231,6 +231,16 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int r = 0; r < 16; ++r) dqacc[db][r] = 0.f;
+    // At D = 128 the dP^T products start from -Delta of the lane's row, held
+    // in every element of a loop-invariant tile (the MFMA's accumulator
+    // input), so that they give dP^T - Delta with no subtraction (32 vector
+    // instructions per tile).  At D = 96 the tile's 16 registers cost more
+    // than that (measured), and D = 64 gains nothing; there dP^T starts from
+    // 0 and Delta is subtracted.
+    constexpr bool kDeltaInit = D == 128;
+    f32x16 ndelta;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) ndelta[r] = kDeltaInit ? -delta : 0.f;
 
     // One tile, one 32-key half kb at a time (32 keys x 32 rows):
     //   S^T = K Q^T and dP^T = V dO^T (MFMA);
@@ -249,12 +259,9 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
         // contributes nothing.
         if constexpr (CAUSAL && decltype(masked)::value)
           if (ks0 > qw0 + 31) continue;
-        f32x16 s, dp;
+        f32x16 s, dp = ndelta;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          s[r] = 0.f;
-          dp[r] = 0.f;
-        }
+        for (int r = 0; r < 16; ++r) s[r] = 0.f;
 #pragma unroll
         for (int c = 0; c < D / 16; ++c) {
           const int o = rr.rm[c] + 32 * kb * P;
@@ -272,7 +279,7 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(BwdArgs a) {
             if constexpr (CAUSAL) pe = t + off > 0 ? 0.f : pe;   // key after query
             pe = u + off >= 0 ? 0.f : pe;                        // key past the end
           }
-          s[r] = pe * (dp[r] - delta);
+          s[r] = kDeltaInit ? pe * dp[r] : pe * (dp[r] - delta);
         }
 #pragma unroll
         for (int c = 0; c < 2; ++c) {

@@ -2,7 +2,7 @@
 // MFMA rate of the chip under full load, against which the kernels' fraction
 // of peak is read.  The quoted dense peak, 2516.6 TFLOP/s, is 256 CUs x
 // 2.4 GHz x 4096 flop per clock per CU, i.e. one v_mfma_f32_32x32x16_bf16
-// (32768 flop) per 8 clocks on each of a CU's four SIMDs.  The kernel runs
+// (32768 flop) per 32 clocks on each of a CU's four SIMDs.  The kernel runs
 // that instruction in independent chains on register operands, with no
 // memory traffic in the loop, so its rate divided by the CU count and the
 // measured graphics clock gives the flop per clock per CU that the chip

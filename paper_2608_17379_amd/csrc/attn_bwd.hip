@@ -502,10 +502,21 @@ __global__ __launch_bounds__(64 * kDkvWaves, 1) void bwd_dkdv_kernel(BwdArgs a) 
       s = mfma32(ld16(q + o), ld16(krd + rr.rm[c]), s);
       dp = mfma32(ld16(dout + o), ld16(vrd + rr.rm[c]), dp);
     }
+    // The first half of the L log2(e) values, then the transposed operands
+    // of the first dV and dK products, whose latency the softmax covers (LDS
+    // reads complete in order).
+    const int rc0 = 16 * (2 * hq) * P;
+    const f32x4 l4a = *reinterpret_cast<const f32x4*>(&lse[32 * hq + 4 * half]);
+    const f32x4 l4b = *reinterpret_cast<const f32x4*>(&lse[32 * hq + 8 + 4 * half]);
+    __builtin_amdgcn_sched_barrier(0);
+    const u32x2 dlo0 = ld_tr(dout + trr.tr[0][0] + rc0), dhi0 = ld_tr(dout + trr.tr[0][1] + rc0);
+    const u32x2 qlo0 = ld_tr(q + trr.tr[0][0] + rc0), qhi0 = ld_tr(q + trr.tr[0][1] + rc0);
+    __builtin_amdgcn_sched_barrier(0);
     const int t = krow - qs0 - 4 * half;   // key minus the lane's first query
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse[32 * hq + 8 * g + 4 * half]);
+      const f32x4 l4 = g == 0 ? l4a : g == 1 ? l4b
+                              : *reinterpret_cast<const f32x4*>(&lse[32 * hq + 8 * g + 4 * half]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = 4 * g + i;
@@ -524,9 +535,12 @@ __global__ __launch_bounds__(64 * kDkvWaves, 1) void bwd_dkdv_kernel(BwdArgs a) 
       const int rc = 16 * (2 * hq + c) * P;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
-        const u32x2 dlo = ld_tr(dout + trr.tr[db][0] + rc), dhi = ld_tr(dout + trr.tr[db][1] + rc);
+        const bool pre = c == 0 && db == 0;
+        const u32x2 dlo = pre ? dlo0 : ld_tr(dout + trr.tr[db][0] + rc);
+        const u32x2 dhi = pre ? dhi0 : ld_tr(dout + trr.tr[db][1] + rc);
         dvacc[db] = mfma32(u32x4{dlo[0], dlo[1], dhi[0], dhi[1]}, pb, dvacc[db]);
-        const u32x2 qlo = ld_tr(q + trr.tr[db][0] + rc), qhi = ld_tr(q + trr.tr[db][1] + rc);
+        const u32x2 qlo = pre ? qlo0 : ld_tr(q + trr.tr[db][0] + rc);
+        const u32x2 qhi = pre ? qhi0 : ld_tr(q + trr.tr[db][1] + rc);
         dkacc[db] = mfma32(u32x4{qlo[0], qlo[1], qhi[0], qhi[1]}, dsb, dkacc[db]);
       }
     }
